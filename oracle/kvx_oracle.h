@@ -1,0 +1,80 @@
+/*
+ * CPU oracle for the shared-KV store/load path -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Only tests/, __graft_entry__.smoke() and the benchmark's CPU-baseline leg
+ * may call this library.  It shares no code, header, table or helper with the
+ * HIP library; the GPU product path never loads it.
+ *
+ * What it computes (the plain definition, exact; no approximation):
+ *   Paper, Sec. 2.2 -- KV state is moved as opaque bytes; full-attention layers
+ *   contribute the K/V pages that precede a prefix boundary.
+ *   Paper, Sec. 3.1 -- a logical chunk spans several paged cache blocks, and the
+ *   chunk length must be a whole number of pages (the paper's instance: a
+ *   1,568-token logical block is 49 pages of 32 tokens).
+ *
+ * Cache element (l, b, kv, h, s, d) sits at byte
+ *     b*block_stride + ((kv*H + h)*BS + s)*D*E + d*E      of layer_ptrs[l]
+ * (per-layer [NB][2][H][BS][D], "HND" as in the paper's Table 1; kv 0 = K).
+ * Token t lives in block bt[t / BS], slot t % BS.
+ * Chunk i (of nc = ceil(n / C)) holds tokens [i*C, i*C + r_i), r_i = min(C, n - i*C),
+ * packed plane-major [L][2][r_i][H][D] at pool + chunk_ids[i]*slot_bytes,
+ * slot_bytes = C * 2*L*H*D*E.  Bytes [r_i*TB, slot_bytes) of a slot are neither
+ * written by pack nor read by unpack.  Unpack is the exact inverse and touches
+ * no cache byte outside the named token slots.
+ */
+#ifndef KVX_ORACLE_H
+#define KVX_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct oracle_layout {
+    int32_t num_layers;   /* L  */
+    int32_t num_kv_heads; /* H  */
+    int32_t head_dim;     /* D  */
+    int32_t elem_bytes;   /* E  */
+    int32_t block_size;   /* BS: tokens per paged block */
+    int32_t chunk_tokens; /* C : tokens per packed chunk */
+} oracle_layout;
+
+/* Error codes (negative). */
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+
+/* Bytes of one packed slot: C * 2*L*H*D*E. Returns -1 on an invalid layout. */
+int64_t oracle_slot_bytes(const oracle_layout *lay);
+
+/*
+ * Validation (Sec. 3.1: layout constraints are checked, never inferred):
+ * positive sizes, E in {1,2,4}, C % BS == 0, n >= 0, block_stride >= 2*H*BS*D*E,
+ * every bt[0 .. ceil(n/BS)) in [0, num_blocks), every chunk id in
+ * [0, num_slots), and (pack only) chunk ids pairwise distinct.
+ * Returns ORACLE_OK or ORACLE_EINVAL.
+ */
+int oracle_validate(const oracle_layout *lay, int64_t num_blocks, int64_t block_stride,
+                    const int32_t *block_table, int64_t n_tokens, int64_t num_slots,
+                    const int64_t *chunk_ids, int for_pack);
+
+/*
+ * Pack (store): copy every named token row of the cache into its chunk row.
+ * layer_ptrs: L host pointers.  pool: num_slots * slot_bytes host bytes.
+ * nthreads >= 1: chunks are split over that many POSIX threads (each chunk is
+ * independent).  Returns ORACLE_OK or ORACLE_EINVAL (nothing written then).
+ */
+int oracle_pack(const oracle_layout *lay, const uint8_t *const *layer_ptrs, int64_t num_blocks,
+                int64_t block_stride, const int32_t *block_table, int64_t n_tokens,
+                uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids, int nthreads);
+
+/* Unpack (load): the exact inverse of oracle_pack. */
+int oracle_unpack(const oracle_layout *lay, uint8_t *const *layer_ptrs, int64_t num_blocks,
+                  int64_t block_stride, const int32_t *block_table, int64_t n_tokens,
+                  const uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids, int nthreads);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVX_ORACLE_H */

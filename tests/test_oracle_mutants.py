@@ -1,0 +1,46 @@
+"""Pin strength: plausible mistakes planted in a copy of the oracle must fail the pins.
+
+Each mutant is a textual edit of ``oracle/kvx_oracle.c`` compiled with gcc into
+a temporary library; the pin suite then runs against it in a subprocess and
+must fail.  Runs on the CPU only (the mistakes are planted in the oracle, never
+in GPU code).
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "kvx_oracle.c")
+
+MUTANTS = {
+    "kv_order_swapped": ("((kv * H + h) * BS + s) * row_bytes", "(((1 - kv) * H + h) * BS + s) * row_bytes"),
+    "plane_stride_C_for_partial": ("chunk_row_offset(lay, r, l, kv, u, h)",
+                                   "chunk_row_offset(lay, lay->chunk_tokens, l, kv, u, h)"),
+    "kv_dropped_in_chunk": ("(((l * 2 + kv) * r + u) * H + h)", "(((l * 2) * r + u) * H + h)"),
+    "chunk_planes_head_major": ("(((l * 2 + kv) * r + u) * H + h)", "(((l * 2 + kv) * H + h) * r + u)"),
+    "slot_off_by_one": ("int64_t s = t % BS;", "int64_t s = (t + 1) % BS;"),
+    "chunk_offset_forgotten": ("job->block_table[t / BS]", "job->block_table[u / BS]"),
+    "unpack_copies_wrong_way": ("memcpy(cache_row, chunk_row, (size_t)row_bytes);",
+                                "memcpy(chunk_row, cache_row, (size_t)row_bytes);"),
+    "divisibility_check_dropped": ("if (lay->chunk_tokens % lay->block_size != 0)", "if (0)"),
+    "head_and_slot_swapped": ("((kv * H + h) * BS + s) * row_bytes", "((kv * BS + s) * H + h) * row_bytes"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"mutation anchor for {name} not found in the oracle source"
+    mutated = tmp_path / "mut.c"
+    mutated.write_text(src.replace(old, new))
+    lib = tmp_path / "libmut.so"
+    subprocess.run(["gcc", "-std=c11", "-O1", "-fPIC", "-shared", "-I", os.path.join(ROOT, "oracle"),
+                    "-o", str(lib), str(mutated), "-lpthread"], check=True)
+    env = dict(os.environ, KVX_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"

@@ -1,0 +1,239 @@
+/*
+ * kvx -- store and load of paged KV state between a GPU KV cache and a pinned
+ * host-memory chunk pool, on AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the state transfer of shared host-memory KV caching between
+ * inference replicas (arxiv 2609.15021): a replica stores the KV pages that
+ * precede a prefix boundary into a shared host tier as packed chunks (Sec. 2,
+ * Fig. 1; Sec. 2.2), and another replica loads them back into its own paged
+ * cache instead of recomputing the prefix (Sec. 5.1).  Every entry point is
+ * ordered against the caller's stream: omitting that dependency is the fault
+ * the paper diagnoses (Sec. 3.2).
+ *
+ * Plain C ABI: no C++ types, no torch types; pointers are explicit host or
+ * device addresses; streams are hipStream_t values passed as void*.  No entry
+ * point throws; all return a kv_status (0 = success, negative = error) unless
+ * stated.  kv_last_error() describes the most recent failure on the calling
+ * thread.
+ *
+ * ---------------------------------------------------------------------------
+ * Byte layout (normative; "E" = elem_bytes, all offsets 64-bit):
+ *
+ *  Cache: layer l is one device buffer layer_ptrs[l] holding num_blocks blocks,
+ *    block b at byte b*block_stride.  Inside a block, element (kv, h, s, d) is at
+ *    ((kv*H + h)*BS + s)*D*E + d*E, i.e. [2][H][BS][D] ("HND", kv 0 = K, 1 = V;
+ *    the paper's replicas run HND, Table 1).  Token t of a prefix lives in block
+ *    block_table[t / BS] at slot t % BS.
+ *
+ *  Chunks: a prefix of n tokens is cut into nc = ceil(n / C) chunks; chunk i
+ *    holds tokens [i*C, i*C + r_i), r_i = min(C, n - i*C) (only the last chunk
+ *    may be partial).  Chunk i is stored in pool slot chunk_ids[i], plane-major
+ *    [L][2][r_i][H][D]: element (l, kv, u, h, d) at
+ *    (((l*2 + kv)*r_i + u)*H + h)*D*E + d*E.  A slot is C*TB bytes, TB = 2*L*H*D*E
+ *    bytes per token; a partial chunk occupies exactly its first r_i*TB bytes and
+ *    the slot's remaining bytes are neither written by kv_store nor read by
+ *    kv_load.  The layout is fixed by this descriptor, never inferred from a
+ *    tensor's rank or shape (the representation fault of Sec. 3.1).
+ *
+ * Ordering contract (Sec. 3.2 and Fig. 2):
+ *  (i)   every device read (store) or write (load) of the cache, and every pool
+ *        access, happens after all work enqueued on `stream` before the call;
+ *  (ii)  work enqueued on `stream` after the call observes all of the call's
+ *        writes (the pool for store, the cache for load);
+ *  (iii) returning from a call establishes nothing: the host may touch the pool
+ *        only after synchronising `stream` (or an event recorded on it after the
+ *        call) -- the paper's host-side completion handling;
+ *  (iv)  use of one pool from two streams is ordered by the caller (event or
+ *        synchronisation), as between two replicas.
+ * ---------------------------------------------------------------------------
+ */
+#ifndef KVX_H
+#define KVX_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Every entry point below is exported; everything else in the library is hidden. */
+#if defined(__GNUC__) || defined(__clang__)
+#define KV_API __attribute__((visibility("default")))
+#else
+#define KV_API
+#endif
+
+typedef int32_t kv_status;
+
+#define KV_OK 0
+#define KV_EINVAL (-1)        /* invalid argument or layout; nothing was enqueued */
+#define KV_ENOMEM (-2)        /* pinned host or device allocation failed; no fallback was taken */
+#define KV_EHIP (-3)          /* a HIP runtime call failed (name and message in kv_last_error) */
+#define KV_EUNSUPPORTED (-4)  /* valid per the definition, but outside what the GPU path handles */
+#define KV_EASYNC (-5)        /* a device-side check failed in an earlier call (kv_pool_async_error) */
+
+/* Host transfer modes (chosen explicitly; nothing is selected silently, cf. Sec. 3.2). */
+#define KV_MODE_ZERO_COPY 1u  /* gather/scatter kernels on `stream` access mapped pinned memory directly */
+#define KV_MODE_STAGED 2u     /* pack/unpack in device staging on `stream`; DMA copies on event-gated side streams */
+
+/* Pool host-memory kinds. */
+#define KV_HOST_COHERENT 0u     /* fine-grained pinned memory (default) */
+#define KV_HOST_NONCOHERENT 1u  /* coarse-grained pinned memory */
+
+/* Async error bits reported by kv_pool_async_error. */
+#define KV_ASYNC_BAD_BLOCK 1   /* a block_table entry was outside [0, num_blocks); that block was skipped */
+
+/* Tokens' geometry; identical for a cache and the pool it talks to. */
+typedef struct kv_layout {
+    int32_t num_layers;   /* L  >= 1 */
+    int32_t num_kv_heads; /* H  >= 1 */
+    int32_t head_dim;     /* D  >= 1 */
+    int32_t elem_bytes;   /* E in {1, 2, 4}; values are moved as opaque bytes */
+    int32_t block_size;   /* BS >= 1: tokens per paged block */
+    int32_t chunk_tokens; /* C  >= 1: tokens per packed chunk; C % BS == 0 (Sec. 3.1) */
+} kv_layout;
+
+/* A replica's paged KV cache.  The caller owns all memory it names. */
+typedef struct kv_cache {
+    kv_layout layout;
+    int32_t num_blocks;          /* blocks per layer buffer */
+    int32_t device;              /* HIP device ordinal the buffers live on */
+    void *const *layer_ptrs;     /* HOST array of num_layers DEVICE pointers, read during the call only */
+    int64_t block_stride_bytes;  /* bytes between blocks; 0 = packed (2*H*BS*D*E) */
+} kv_cache;
+
+/* Pool creation options.  Zero-initialised fields take the documented defaults. */
+typedef struct kv_pool_options {
+    uint32_t mode;             /* KV_MODE_ZERO_COPY or KV_MODE_STAGED (required, no default) */
+    uint32_t host_kind;        /* KV_HOST_COHERENT (0) or KV_HOST_NONCOHERENT */
+    int32_t staging_slots;     /* staged ring depth K >= 2 (default 3); with mode zero-copy, > 0
+                                  also allocates staging so kv_pool_set_mode can switch later */
+    int32_t chunks_per_batch;  /* chunks per staging slot / per kernel launch, 1..256 (default 8
+                                  staged, 256 zero-copy) */
+    int32_t side_streams;      /* staged: DMA side streams, 1..8 (default 2) */
+    int32_t profile;           /* nonzero: time every pack/unpack launch (kv_pool_kernel_stats) */
+} kv_pool_options;
+
+typedef struct kv_pool kv_pool;
+
+typedef struct kv_pool_info {
+    int64_t num_slots;
+    int64_t slot_bytes;        /* C * TB */
+    int64_t pool_bytes;        /* num_slots * slot_bytes, pinned as one region */
+    int64_t staging_bytes;     /* device staging (0 without staging) */
+    double alloc_seconds;      /* wall time of the pinned allocation (cf. Sec. 3.3) */
+    int32_t device;
+    uint32_t mode;
+    uint32_t host_kind;
+    int32_t is_pinned;         /* 1: the runtime reports the pool as pinned host memory */
+    int32_t staging_slots;
+    int32_t chunks_per_batch;
+    int32_t side_streams;
+    int32_t reserved;
+    void *host_base;           /* host address of slot 0 */
+    void *device_base;         /* device address of slot 0 (mapped pinned memory) */
+} kv_pool_info;
+
+/*
+ * kv_pool_create -- allocate the shared host tier (Sec. 2: a host-RAM pool
+ * shared by the replicas; Sec. 3.3: the full pool must really be pinned).
+ * Pins exactly num_slots * slot_bytes bytes as ONE region (Sec. 3.2 notes a
+ * workaround registering the whole pool together), mapped for device access,
+ * verifies with the runtime that it is pinned, and times the allocation.  On
+ * the current HIP device it creates the staging ring, side streams (default
+ * priority, non-blocking) and events.  Never falls back to pageable memory:
+ * failure is KV_ENOMEM.  *out receives the pool (owned by the library until
+ * kv_pool_destroy).  Errors: KV_EINVAL (layout, num_slots <= 0, options),
+ * KV_ENOMEM, KV_EHIP.
+ */
+KV_API kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_pool_options *opts,
+                         kv_pool **out);
+
+/* Waits for the pool's own side streams, then frees everything.  NULL is a no-op. */
+KV_API kv_status kv_pool_destroy(kv_pool *pool);
+
+/* Fills *info.  KV_EINVAL on NULL arguments. */
+KV_API kv_status kv_pool_get_info(const kv_pool *pool, kv_pool_info *info);
+
+/* Host address of a slot (NULL if out of range).  Touch it only when no call using it is in flight. */
+KV_API void *kv_pool_slot(kv_pool *pool, int64_t slot);
+KV_API int64_t kv_pool_slot_bytes(const kv_pool *pool);  /* -1 on NULL */
+KV_API int64_t kv_pool_num_slots(const kv_pool *pool);   /* -1 on NULL */
+
+/* Switch mode between calls.  KV_EINVAL for an unknown mode or staged mode without staging. */
+KV_API kv_status kv_pool_set_mode(kv_pool *pool, uint32_t mode);
+
+/*
+ * Device-side faults seen since the last clear (bitmask of KV_ASYNC_*; 0 if
+ * none), meaningful after the caller has synchronised the streams it used.  A
+ * zero result is not an integrity check (Sec. 1: success signals are not).
+ * clear != 0 resets the word.  Returns the mask, or KV_EINVAL on NULL.
+ */
+KV_API int32_t kv_pool_async_error(kv_pool *pool, int clear);
+
+/*
+ * Accumulated pack (which = 0) or unpack (which = 1) kernel time of a pool
+ * created with opts.profile != 0.  Call after synchronising the streams used;
+ * each launch's start/end events were recorded on the caller stream around it.
+ * *launches, *total_ms and *bytes (algorithmic bytes: payload read + written)
+ * receive the totals since the last reset (reset != 0 clears them).
+ */
+KV_API kv_status kv_pool_kernel_stats(kv_pool *pool, int which, int reset, int64_t *launches, double *total_ms,
+                               double *bytes);
+
+/*
+ * Host-only validation of a store/load request, no HIP call (Sec. 3.1: layout
+ * constraints are validated, never inferred).  Checks: cache layout equals
+ * pool_layout field by field; positive sizes; E in {1,2,4}; C % BS == 0;
+ * block_stride 0 or >= 2*H*BS*D*E; n_tokens >= 0; for n_tokens > 0 non-NULL
+ * layer pointers and chunk_ids, chunk ids in [0, pool_slots), and for a store
+ * pairwise distinct (duplicates make the result order dependent).  GPU-path
+ * limits give KV_EUNSUPPORTED: D*E % 16 != 0, a layer pointer or
+ * block_stride not 16-byte aligned, more than 2^31-1 slots.
+ * Returns KV_OK / KV_EINVAL / KV_EUNSUPPORTED with kv_last_error set.
+ */
+KV_API kv_status kv_check(const kv_cache *cache, const kv_layout *pool_layout, int64_t pool_slots,
+                   int64_t n_tokens, const int64_t *chunk_ids, int for_store);
+
+/*
+ * kv_store -- store (Sec. 2.2: the K/V pages preceding a prefix boundary, as
+ * opaque bytes) the first n_tokens tokens of `cache`, addressed through
+ * block_table, into pool slots chunk_ids[0 .. nc) in the chunk layout above.
+ *   block_table: DEVICE int32[ceil(n_tokens / BS)], owned by the caller, valid
+ *                and unmodified until the call completes on `stream`;
+ *   chunk_ids:   HOST int64[nc], read before return;
+ *   stream:      hipStream_t (NULL = the null stream).
+ * Enqueues only: never blocks the host on device work.  n_tokens == 0 is a
+ * no-op.  Argument errors return before anything is enqueued.  An entry of
+ * block_table outside [0, num_blocks) is skipped on the device and flagged in
+ * kv_pool_async_error.  Calls on one pool are serialised internally.
+ */
+KV_API kv_status kv_store(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, kv_pool *pool,
+                   const int64_t *chunk_ids, void *stream);
+
+/*
+ * kv_load -- the exact inverse of kv_store into `cache` (Sec. 5.1: the receiving
+ * replica restores the shared prefix instead of recomputing it).  Writes only
+ * the token slots named by (block_table, n_tokens); every other cache byte is
+ * untouched, including slots s >= n % BS of a partial last block.
+ * Destination blocks must be distinct (precondition; otherwise the result
+ * depends on write order).  Duplicate chunk ids are allowed (they are reads).
+ * Ownership, ordering and errors as kv_store.
+ */
+KV_API kv_status kv_load(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, kv_pool *pool,
+                  const int64_t *chunk_ids, void *stream);
+
+/* Thread-local text of the last failure on this thread (HIP error name, message, call site). */
+KV_API const char *kv_last_error(void);
+
+/* Name of a status code ("KV_OK", "KV_EINVAL", ...). */
+KV_API const char *kv_status_name(kv_status status);
+
+/* Library version string. */
+KV_API const char *kv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVX_H */

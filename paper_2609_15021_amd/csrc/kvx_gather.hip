@@ -1,0 +1,171 @@
+// Pack (store) and unpack (load) kernels for gfx950.
+//
+// One workgroup moves one slab: the (layer l, K/V, block j) piece of chunk i, i.e. the
+// bs <= BS tokens of one paged block for one layer and one of K/V.  On the cache side the
+// slab is the contiguous [H][BS][D] region of that block (HND, the paper's replica layout,
+// Table 1); on the chunk side it is the contiguous [bs][H][D] run of token-major rows
+// inside plane (l, kv) of the chunk.  The slab is therefore contiguous on both sides and
+// differs only by a permutation of D*E-byte rows: cache row (h, s) <-> chunk row (s, h).
+//
+// Lanes walk the chunk side in order (16 consecutive lanes cover one 256-byte row when
+// D*E = 256), so the pool/staging side -- host memory over PCIe in zero-copy mode -- is
+// touched in fully contiguous 1 KiB-per-wave runs, and the cache side in whole-row
+// 256-byte runs.  Rows are >= 16 bytes and moved as 16-byte vectors, so no LDS transpose
+// is needed for coalescing.  Values are moved as integers only: no float register ever
+// holds them (NaN payloads, -0 and subnormals survive).
+//
+// Each thread keeps U vectors in flight (U loads issued before the U stores).  Index math
+// is wave-uniform except one division at thread start; afterwards every step is an
+// addition with carry.
+#include "kvx_internal.h"
+
+namespace kvx {
+
+namespace {
+
+// One 16-byte vector as a native 128-bit register tuple (kept in VGPRs; never a float).
+typedef uint32_t vec16 __attribute__((ext_vector_type(4)));
+
+// Walks chunk-order vector indices v = t, t + kThreads, t + 2*kThreads, ... of one slab,
+// maintaining (s, h, col) with v = (s*H + h)*VR + col.
+struct RowWalker {
+    int s, h, col;
+    int VR, H;
+    int dcol, ds0, dh0, ds1, dh1;  // per-step increments (without / with a column carry)
+
+    __device__ RowWalker(int v, int vec_per_row, int heads) : VR(vec_per_row), H(heads) {
+        int q = v / VR;
+        col = v - q * VR;
+        s = q / H;
+        h = q - s * H;
+        int dq = kThreads / VR;
+        dcol = kThreads - dq * VR;
+        ds0 = dq / H;
+        dh0 = dq - ds0 * H;
+        ds1 = (dq + 1) / H;
+        dh1 = (dq + 1) - ds1 * H;
+    }
+
+    __device__ void advance() {
+        col += dcol;
+        int ds = ds0, dh = dh0;
+        if (col >= VR) {
+            col -= VR;
+            ds = ds1;
+            dh = dh1;
+        }
+        h += dh;
+        s += ds;
+        if (h >= H) {
+            h -= H;
+            s += 1;
+        }
+    }
+
+    // 16-byte-vector offset of the current element inside the cache-side [H][BS][D] slab.
+    __device__ int cache_vec(int BS) const { return (h * BS + s) * VR + col; }
+};
+
+template <int DIR, int U>
+__global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
+    // Workgroup -> (chunk c, layer ll, kv, block j); j varies fastest so consecutive
+    // workgroups write consecutive chunk-side regions.
+    const int bpc = a.blocks_per_chunk;
+    const int64_t wg = blockIdx.x;
+    const int j = static_cast<int>(wg % bpc);
+    int64_t rest = wg / bpc;
+    const int kv = static_cast<int>(rest & 1);
+    rest >>= 1;
+    const int ll = static_cast<int>(rest % a.nlayers);
+    const int c = static_cast<int>(rest / a.nlayers);
+
+    const int64_t i = a.chunk0 + c;  // global chunk index
+    const int64_t remaining = a.n_tokens - i * a.C;
+    const int64_t r = remaining < a.C ? remaining : a.C;  // tokens in chunk i
+    const int64_t tok0 = static_cast<int64_t>(j) * a.BS;  // first token of the slab in the chunk
+    if (tok0 >= r)
+        return;
+    const int bs = static_cast<int>((r - tok0) < a.BS ? (r - tok0) : a.BS);
+
+    const int32_t b = a.block_table[i * bpc + j];
+    if (b < 0 || b >= a.num_blocks) {
+        if (threadIdx.x == 0)
+            __hip_atomic_store(a.err, KV_ASYNC_BAD_BLOCK, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        return;
+    }
+
+    const int l = a.layer0 + ll;
+    const int64_t row_bytes = static_cast<int64_t>(a.vec_per_row) * 16;
+    uint8_t *cache_slab = a.layer[ll] + static_cast<int64_t>(b) * a.block_stride +
+                          static_cast<int64_t>(kv) * a.H * a.BS * row_bytes;
+    uint8_t *chunk_slab = a.chunk_base + static_cast<int64_t>(a.slot[c]) * a.slot_stride +
+                          ((static_cast<int64_t>(l) * 2 + kv) * r + tok0) * a.H * row_bytes;
+
+    vec16 *cache_v = reinterpret_cast<vec16 *>(cache_slab);
+    vec16 *chunk_v = reinterpret_cast<vec16 *>(chunk_slab);
+    const int nvec = bs * a.H * a.vec_per_row;
+
+    RowWalker w(threadIdx.x, a.vec_per_row, a.H);
+    const int tid = static_cast<int>(threadIdx.x);
+    int base = 0;  // first chunk-side vector of the current tile (uniform across the workgroup)
+    // Full tiles: every thread has U in-range vectors; all U loads issue before any store.
+    for (; base + kThreads * U <= nvec; base += kThreads * U) {
+        const int v = base + tid;
+        int cache_off[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            cache_off[u] = w.cache_vec(a.BS);
+            w.advance();
+        }
+        vec16 buf[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (DIR == kPack)
+                buf[u] = cache_v[cache_off[u]];
+            else
+                buf[u] = chunk_v[v + u * kThreads];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (DIR == kPack)
+                chunk_v[v + u * kThreads] = buf[u];
+            else
+                cache_v[cache_off[u]] = buf[u];
+        }
+    }
+    // Tail: one vector at a time.
+    for (int v = base + tid; v < nvec; v += kThreads) {
+        const int co = w.cache_vec(a.BS);
+        w.advance();
+        if (DIR == kPack)
+            chunk_v[v] = cache_v[co];
+        else
+            cache_v[co] = chunk_v[v];
+    }
+}
+
+constexpr int kUnroll = 8;
+
+}  // namespace
+
+int max_chunks_per_launch(const Geometry &g, int nlayers) {
+    const int64_t wgs_per_chunk = static_cast<int64_t>(nlayers) * 2 * g.blocks_per_chunk;
+    const int64_t max_wgs = (int64_t{1} << 31) / kThreads - 1;
+    int64_t m = max_wgs / wgs_per_chunk;
+    if (m > kMaxLaunchChunks)
+        m = kMaxLaunchChunks;
+    return static_cast<int>(m < 1 ? 1 : m);
+}
+
+hipError_t launch_gather(const GatherArgs &args, Direction dir, hipStream_t stream) {
+    const int64_t grid = static_cast<int64_t>(args.nchunks) * args.nlayers * 2 * args.blocks_per_chunk;
+    if (grid <= 0)
+        return hipSuccess;
+    // hipLaunchKernel reports launch failures directly (no sticky last-error state).
+    const void *fn = dir == kPack ? reinterpret_cast<const void *>(&gather_kernel<kPack, kUnroll>)
+                                  : reinterpret_cast<const void *>(&gather_kernel<kUnpack, kUnroll>);
+    void *kargs[] = {const_cast<GatherArgs *>(&args)};
+    return hipLaunchKernel(fn, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), kargs, 0, stream);
+}
+
+}  // namespace kvx

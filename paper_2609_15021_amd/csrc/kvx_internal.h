@@ -1,0 +1,120 @@
+// Internal declarations shared by the kvx host code and kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kvx.h"
+
+namespace kvx {
+
+constexpr int kThreads = 256;          // work-items per workgroup (4 wave64s)
+constexpr int kMaxLaunchLayers = 64;   // layer pointers carried in one launch's kernel arguments
+constexpr int kMaxLaunchChunks = 256;  // slot ids carried in one launch's kernel arguments
+
+// Derived sizes of a layout (all bytes, 64-bit).
+struct Geometry {
+    int64_t L, H, D, E, BS, C;
+    int64_t row_bytes;     // D*E: one (head, token) row
+    int64_t vec_per_row;   // row_bytes / 16
+    int64_t block_bytes;   // 2*H*BS*D*E
+    int64_t block_stride;  // bytes between blocks in a layer buffer
+    int64_t token_bytes;   // TB = 2*L*H*D*E
+    int64_t slot_bytes;    // C*TB
+    int64_t blocks_per_chunk;  // C / BS
+};
+
+Geometry geometry(const kv_layout &lay, int64_t block_stride_bytes);
+
+// Kernel arguments of one gather (pack) or scatter (unpack) launch.  A launch covers
+// chunks [chunk0, chunk0 + nchunks) of the prefix and layers [layer0, layer0 + nlayers).
+// Passed by value so that every pointer and id is captured at enqueue time.
+struct GatherArgs {
+    uint8_t *layer[kMaxLaunchLayers];  // cache layer base pointers (device) of layers layer0..
+    uint8_t *chunk_base;               // device-visible address of slot 0 (pool or staging)
+    const int32_t *block_table;        // device int32[ceil(n/BS)]
+    int32_t *err;                      // device-visible async error word
+    int64_t slot_stride;               // bytes between slot ids at chunk_base
+    int64_t block_stride;
+    int64_t n_tokens;                  // prefix length (for r_i of every chunk)
+    int64_t chunk0;                    // global index of the launch's first chunk
+    int32_t num_blocks;
+    int32_t layer0, nlayers;
+    int32_t H, BS, C;
+    int32_t vec_per_row;
+    int32_t blocks_per_chunk;
+    int32_t nchunks;
+    int32_t slot[kMaxLaunchChunks];    // slot id of each chunk of the launch
+};
+
+enum Direction { kPack = 0, kUnpack = 1 };
+
+// Enqueue one launch on `stream`.  Returns the launch error (hipSuccess on success).
+hipError_t launch_gather(const GatherArgs &args, Direction dir, hipStream_t stream);
+
+// Largest chunk count per launch that keeps the grid within the 32-bit work-item limit.
+int max_chunks_per_launch(const Geometry &g, int nlayers);
+
+// Thread-local error reporting.
+kv_status fail(kv_status code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+kv_status hip_fail(hipError_t err, const char *what, const char *file, int line);
+void set_last_error(const std::string &msg);
+
+#define KVX_HIP(expr)                                                         \
+    do {                                                                      \
+        hipError_t kvx_e_ = (expr);                                           \
+        if (kvx_e_ != hipSuccess)                                             \
+            return ::kvx::hip_fail(kvx_e_, #expr, __FILE__, __LINE__);        \
+    } while (0)
+
+// Host-only request validation shared by kv_check, kv_store and kv_load.
+kv_status check_layout(const kv_layout &lay);
+kv_status check_request(const kv_cache *cache, const kv_layout *pool_layout, int64_t pool_slots,
+                        int64_t n_tokens, const int64_t *chunk_ids, int for_store);
+
+}  // namespace kvx
+
+// The pool: one pinned host region plus the staging ring and its streams/events.
+struct kv_pool {
+    kv_layout layout{};
+    kvx::Geometry geo{};
+    int64_t num_slots = 0, pool_bytes = 0;
+    int device = 0;
+    uint32_t mode = 0, host_kind = 0;
+    uint8_t *host_base = nullptr;   // host address of slot 0
+    uint8_t *dev_base = nullptr;    // device address of slot 0
+    int32_t *err_host = nullptr;    // async error word (pinned, mapped)
+    int32_t *err_dev = nullptr;
+    double alloc_seconds = 0.0;
+    bool pinned = false;
+
+    // Staging ring (staged mode).
+    int K = 0, cpb = 0, S = 0;
+    uint8_t *staging = nullptr;     // K slots of cpb*slot_bytes each
+    std::vector<hipStream_t> sides;
+    std::vector<hipEvent_t> ev_free;   // staging slot k may be overwritten once this completes
+    std::vector<bool> free_recorded;
+    std::vector<hipEvent_t> ev_ready;  // staging slot k holds the current batch
+    std::vector<hipEvent_t> ev_join;   // per side stream: exit join of a store
+    hipEvent_t ev_entry = nullptr;     // entry gate of a load
+    int ring = 0;
+    int zc_chunks = 0;                 // chunks per zero-copy launch
+
+    // Profiling of pack/unpack launches.
+    bool profile = false;
+    struct Timed {
+        hipEvent_t start, stop;
+        double bytes;
+    };
+    std::vector<Timed> pending[2];
+    std::vector<hipEvent_t> spare_events;
+    int64_t launches[2] = {0, 0};
+    double total_ms[2] = {0.0, 0.0};
+    double total_bytes[2] = {0.0, 0.0};
+
+    std::mutex mu;
+};

@@ -1,0 +1,269 @@
+"""Python binding of the kvx C ABI (``include/kvx.h``): argument marshalling only.
+
+Every step of store and load runs in the HIP library ``libkvx.so``; this module
+only converts torch tensors, numpy arrays and streams into the plain pointers
+and sizes the C ABI takes.  The names are the C ABI's.
+
+The library must bind to the HIP runtime that torch loaded, so torch is
+imported before the library is opened.  If ``libkvx.so`` is missing the import
+fails loudly: there is no CPU or Python fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # noqa: F401  (must precede the library: it provides the process's HIP runtime)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvx.so")
+
+KV_OK = 0
+KV_EINVAL = -1
+KV_ENOMEM = -2
+KV_EHIP = -3
+KV_EUNSUPPORTED = -4
+KV_EASYNC = -5
+
+KV_MODE_ZERO_COPY = 1
+KV_MODE_STAGED = 2
+KV_HOST_COHERENT = 0
+KV_HOST_NONCOHERENT = 1
+KV_ASYNC_BAD_BLOCK = 1
+
+MODES = {"zero_copy": KV_MODE_ZERO_COPY, "staged": KV_MODE_STAGED}
+
+
+class KvLayout(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("elem_bytes", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("chunk_tokens", ctypes.c_int32)]
+
+
+class KvCache(ctypes.Structure):
+    _fields_ = [("layout", KvLayout), ("num_blocks", ctypes.c_int32), ("device", ctypes.c_int32),
+                ("layer_ptrs", ctypes.POINTER(ctypes.c_void_p)), ("block_stride_bytes", ctypes.c_int64)]
+
+
+class KvPoolOptions(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_uint32), ("host_kind", ctypes.c_uint32),
+                ("staging_slots", ctypes.c_int32), ("chunks_per_batch", ctypes.c_int32),
+                ("side_streams", ctypes.c_int32), ("profile", ctypes.c_int32)]
+
+
+class KvPoolInfo(ctypes.Structure):
+    _fields_ = [("num_slots", ctypes.c_int64), ("slot_bytes", ctypes.c_int64),
+                ("pool_bytes", ctypes.c_int64), ("staging_bytes", ctypes.c_int64),
+                ("alloc_seconds", ctypes.c_double), ("device", ctypes.c_int32),
+                ("mode", ctypes.c_uint32), ("host_kind", ctypes.c_uint32),
+                ("is_pinned", ctypes.c_int32), ("staging_slots", ctypes.c_int32),
+                ("chunks_per_batch", ctypes.c_int32), ("side_streams", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("host_base", ctypes.c_void_p),
+                ("device_base", ctypes.c_void_p)]
+
+
+class KvError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+def _open():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"kvx HIP library not built ({LIB_PATH} missing); run __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
+    sig = {
+        "kv_pool_create": ([ctypes.POINTER(KvLayout), i64, ctypes.POINTER(KvPoolOptions), ctypes.POINTER(P)], i32),
+        "kv_pool_destroy": ([P], i32),
+        "kv_pool_get_info": ([P, ctypes.POINTER(KvPoolInfo)], i32),
+        "kv_pool_slot": ([P, i64], P),
+        "kv_pool_slot_bytes": ([P], i64),
+        "kv_pool_num_slots": ([P], i64),
+        "kv_pool_set_mode": ([P, u32], i32),
+        "kv_pool_async_error": ([P, ctypes.c_int], i32),
+        "kv_pool_kernel_stats": ([P, ctypes.c_int, ctypes.c_int, ctypes.POINTER(i64),
+                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)], i32),
+        "kv_check": ([ctypes.POINTER(KvCache), ctypes.POINTER(KvLayout), i64, i64, P, ctypes.c_int], i32),
+        "kv_store": ([ctypes.POINTER(KvCache), P, i64, P, P, P], i32),
+        "kv_load": ([ctypes.POINTER(KvCache), P, i64, P, P, P], i32),
+        "kv_last_error": ([], ctypes.c_char_p),
+        "kv_status_name": ([i32], ctypes.c_char_p),
+        "kv_version": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+_lib = _open()
+
+EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slot", "kv_pool_slot_bytes",
+           "kv_pool_num_slots", "kv_pool_set_mode", "kv_pool_async_error", "kv_pool_kernel_stats", "kv_check",
+           "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version")
+
+
+def kv_last_error() -> str:
+    return _lib.kv_last_error().decode()
+
+
+def kv_status_name(status: int) -> str:
+    return _lib.kv_status_name(int(status)).decode()
+
+
+def kv_version() -> str:
+    return _lib.kv_version().decode()
+
+
+def _raise(status: int):
+    if status != KV_OK:
+        raise KvError(status, f"{kv_status_name(status)}: {kv_last_error()}")
+
+
+def make_layout(L, H, D, E, BS, C) -> KvLayout:
+    return KvLayout(int(L), int(H), int(D), int(E), int(BS), int(C))
+
+
+class Cache:
+    """A replica's paged cache as the C ABI sees it (keeps the tensors and pointer array alive).
+
+    ``layers``: one tensor [L][NB][2][H][BS][D] (any dtype of elem_bytes), or a list of L
+    per-layer tensors [NB][...]; ``block_stride_bytes`` 0 means packed blocks.
+    """
+
+    def __init__(self, layers, layout: KvLayout, num_blocks: int, block_stride_bytes: int = 0):
+        if isinstance(layers, torch.Tensor):
+            tensors = [layers[l] for l in range(layers.shape[0])]
+            self._keep = [layers]
+        else:
+            tensors = list(layers)
+            self._keep = tensors
+        if len(tensors) != layout.num_layers:
+            raise ValueError(f"{len(tensors)} layer buffers for a {layout.num_layers}-layer layout")
+        dev = tensors[0].device
+        if dev.type != "cuda":
+            raise ValueError("cache layers must be device tensors")
+        block_bytes = 2 * layout.num_kv_heads * layout.block_size * layout.head_dim * layout.elem_bytes
+        need = int(num_blocks) * int(block_stride_bytes or block_bytes)
+        for k, t in enumerate(tensors):
+            if t.device != dev or not t.is_contiguous() or t.numel() * t.element_size() < need:
+                raise ValueError(f"layer {k}: need a contiguous device buffer of >= {need} bytes on {dev}")
+        self._ptrs = (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+        self.struct = KvCache(layout, int(num_blocks), int(dev.index if dev.index is not None else 0),
+                              ctypes.cast(self._ptrs, ctypes.POINTER(ctypes.c_void_p)), int(block_stride_bytes))
+        self.layout = layout
+
+
+class Pool:
+    """Owning handle of a kv_pool (destroyed by ``kv_pool_destroy`` or garbage collection)."""
+
+    def __init__(self, handle: ctypes.c_void_p, layout: KvLayout):
+        self.handle = handle
+        self.layout = layout
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            try:
+                _lib.kv_pool_destroy(self.handle)
+            except Exception:
+                pass
+            self.handle = None
+
+
+def _stream_handle(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, (torch.cuda.Stream, torch.cuda.ExternalStream)):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def kv_pool_create(layout: KvLayout, num_slots: int, mode="staged", host_kind=KV_HOST_COHERENT,
+                   staging_slots=0, chunks_per_batch=0, side_streams=0, profile=False) -> Pool:
+    m = MODES[mode] if isinstance(mode, str) else int(mode)
+    opts = KvPoolOptions(m, int(host_kind), int(staging_slots), int(chunks_per_batch), int(side_streams),
+                         1 if profile else 0)
+    out = ctypes.c_void_p()
+    _raise(_lib.kv_pool_create(ctypes.byref(layout), int(num_slots), ctypes.byref(opts), ctypes.byref(out)))
+    return Pool(out, layout)
+
+
+def kv_pool_destroy(pool: Pool) -> None:
+    h, pool.handle = pool.handle, None
+    _raise(_lib.kv_pool_destroy(h))
+
+
+def kv_pool_get_info(pool: Pool) -> dict:
+    info = KvPoolInfo()
+    _raise(_lib.kv_pool_get_info(pool.handle, ctypes.byref(info)))
+    return {name: getattr(info, name) for name, _ in KvPoolInfo._fields_}
+
+
+def kv_pool_slot(pool: Pool, slot: int) -> int:
+    return _lib.kv_pool_slot(pool.handle, int(slot)) or 0
+
+
+def kv_pool_slot_bytes(pool: Pool) -> int:
+    return int(_lib.kv_pool_slot_bytes(pool.handle))
+
+
+def kv_pool_num_slots(pool: Pool) -> int:
+    return int(_lib.kv_pool_num_slots(pool.handle))
+
+
+def kv_pool_set_mode(pool: Pool, mode) -> None:
+    _raise(_lib.kv_pool_set_mode(pool.handle, MODES[mode] if isinstance(mode, str) else int(mode)))
+
+
+def kv_pool_async_error(pool: Pool, clear: bool = False) -> int:
+    return int(_lib.kv_pool_async_error(pool.handle, 1 if clear else 0))
+
+
+def kv_pool_kernel_stats(pool: Pool, which: str, reset: bool = False):
+    """(launches, total_ms, algorithmic_bytes) of the pack or unpack kernels since the last reset."""
+    n, ms, b = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double()
+    _raise(_lib.kv_pool_kernel_stats(pool.handle, {"pack": 0, "unpack": 1}[which], 1 if reset else 0,
+                                     ctypes.byref(n), ctypes.byref(ms), ctypes.byref(b)))
+    return int(n.value), float(ms.value), float(b.value)
+
+
+def pool_view(pool: Pool) -> np.ndarray:
+    """The whole pinned pool as a host uint8 numpy array (touch only when no call is in flight)."""
+    info = kv_pool_get_info(pool)
+    buf = (ctypes.c_uint8 * info["pool_bytes"]).from_address(info["host_base"])
+    return np.ctypeslib.as_array(buf)
+
+
+def _chunk_ids(chunk_ids):
+    a = np.ascontiguousarray(np.asarray(chunk_ids, dtype=np.int64))
+    return a, (ctypes.c_void_p(a.ctypes.data) if a.size else None)
+
+
+def _block_table_ptr(block_table, cache: Cache):
+    if block_table is None:
+        return None
+    if not isinstance(block_table, torch.Tensor) or block_table.dtype != torch.int32 or \
+            block_table.device.type != "cuda" or not block_table.is_contiguous():
+        raise TypeError("block_table must be a contiguous int32 device tensor")
+    return ctypes.c_void_p(block_table.data_ptr())
+
+
+def kv_check(cache: Cache, pool_layout: KvLayout, pool_slots: int, n_tokens: int, chunk_ids, for_store: bool) -> int:
+    ids, ptr = _chunk_ids(chunk_ids) if chunk_ids is not None else (None, None)
+    return int(_lib.kv_check(ctypes.byref(cache.struct), ctypes.byref(pool_layout), int(pool_slots), int(n_tokens),
+                             ptr, 1 if for_store else 0))
+
+
+def kv_store(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, stream=None) -> None:
+    ids, ptr = _chunk_ids(chunk_ids)
+    _raise(_lib.kv_store(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
+                         pool.handle, ptr, _stream_handle(stream)))
+
+
+def kv_load(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, stream=None) -> None:
+    ids, ptr = _chunk_ids(chunk_ids)
+    _raise(_lib.kv_load(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
+                        pool.handle, ptr, _stream_handle(stream)))

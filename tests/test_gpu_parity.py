@@ -1,0 +1,236 @@
+"""GPU parity: kv_store / kv_load through the C ABI, byte-compared with the CPU oracle.
+
+Inputs come from the seeded host generator; expected pool and cache bytes come
+from the oracle applied to those host inputs.  The bar is bit-exact: this path
+moves integers (opaque bytes), so any difference is a failure.
+"""
+import numpy as np
+import pytest
+import torch
+
+import harness
+from paper_2609_15021_amd import kvx
+from tests.gpu_support import (DEV, TINY, Layout, bt_tensor, device_cache, first_mismatch, host_cache,
+                               oracle_pool, oracle_unpack_into, to_device, to_host)
+
+pytestmark = pytest.mark.gpu
+
+POOL_SENT = 0xA5
+CACHE_SENT = 0x5A
+
+
+def _round_trip(lay: Layout, NB: int, n: int, mode: str, host_kind=0, shuffled=False, dist="u11", seed_tag="t",
+                extra_slots=2, stream=None, block_stride=0, **pool_kw):
+    """Store A -> pool -> load into B (second allocation); compare both with the oracle."""
+    seed = harness.sub_seed("parity", seed_tag, n, lay.L, lay.H, lay.D, lay.E, lay.BS, lay.C)
+    A = host_cache(lay, NB, seed, dist)
+    nblk = lay.nblk(n)
+    btA = harness.block_table(seed + 1, NB, nblk)
+    btB = harness.block_table(seed + 2, NB, nblk)
+    nc = lay.nc(n)
+    num_slots = nc + extra_slots
+    cid = harness.chunk_ids(nc, num_slots, seed + 3 if shuffled else None)
+    pool = kvx.kv_pool_create(lay.kv, num_slots, mode, host_kind=host_kind, **pool_kw)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    dA = to_device(A)
+    dB = device_cache(lay, NB, fill=CACHE_SENT)
+    cA, cB = kvx.Cache(dA, lay.kv, NB), kvx.Cache(dB, lay.kv, NB)
+    tA, tB = bt_tensor(btA), bt_tensor(btB)
+    s = stream if stream is not None else torch.cuda.Stream()
+    kvx.kv_store(cA, tA, n, pool, cid, s)
+    torch.cuda.synchronize()
+    want_pool = oracle_pool(lay, A, btA, n, cid, num_slots, POOL_SENT)
+    assert np.array_equal(view, want_pool), "pool: " + first_mismatch(view, want_pool)
+    kvx.kv_load(cB, tB, n, pool, cid, s)
+    torch.cuda.synchronize()
+    B0 = np.full_like(A, 0).view(np.uint8)
+    B0[:] = CACHE_SENT
+    want_B = oracle_unpack_into(lay, B0.view(A.dtype).reshape(A.shape), btB, n, want_pool, cid)
+    got_B = to_host(dB, A)
+    assert np.array_equal(got_B, want_B), "cache B: " + first_mismatch(got_B, want_B)
+    np.testing.assert_array_equal(to_host(dA, A), A)  # store never writes the source
+    assert kvx.kv_pool_async_error(pool) == 0
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+@pytest.mark.parametrize("host_kind", [kvx.KV_HOST_COHERENT, kvx.KV_HOST_NONCOHERENT])
+@pytest.mark.parametrize("shuffled", [False, True])
+def test_tiny_config_round_trip(mode, host_kind, shuffled):
+    """2 layers, 2 KV heads, D 64, BS 16, bf16 U[-1,1]; 4,096 tokens on 256 random blocks of 512;
+    16 chunks of 256 tokens; load into a different random 256-block set of a second allocation."""
+    _round_trip(TINY, 512, 4096, mode, host_kind, shuffled)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+@pytest.mark.parametrize("n", [4096 + 192, 4096 + 128, 4096 + 64, 4096 + 1, 4, 17, 1, 255, 257])
+def test_partial_chunks_and_blocks(mode, n):
+    """Partial final chunk (compact r*TB bytes, slot tail untouched) and partial final block."""
+    _round_trip(TINY, 512, n, mode, shuffled=True)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+@pytest.mark.parametrize("dims", [
+    (70, 1, 8, 2, 16, 256),     # more layers than one launch carries; 16-byte rows
+    (3, 3, 24, 2, 16, 256),     # 48-byte rows (3 vectors), 3 heads
+    (2, 2, 4, 4, 1, 8),         # E = 4, one-token blocks, tiny chunks
+    (16, 4, 256, 1, 32, 1568),  # the paper's attention geometry: FP8, 4 KV heads, D 256, 32-token pages,
+                                # 1,568-token chunks (Table 1 and Sec. 3.1)
+    (1, 8, 128, 2, 16, 16),     # chunk == block
+    (2, 1, 2048, 2, 4, 64),     # 4 KiB rows (more vectors per row than work-items)
+])
+def test_layout_variants(mode, dims):
+    lay = Layout(*dims)
+    n = (2 if lay.C > 256 else 3) * lay.C + lay.BS + 1
+    NB = lay.nblk(n) + 7
+    _round_trip(lay, NB, n, mode, shuffled=True, dist="raw", staging_slots=2, chunks_per_batch=2)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_all_16bit_patterns_bit_exact(mode):
+    """Raw bit patterns (NaN payloads, +-Inf, -0, subnormals as bf16) survive the GPU path."""
+    _round_trip(TINY, 512, 4096, mode, dist="raw", seed_tag="raw")
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_small_staging_ring_many_batches(mode):
+    """A 2-slot staging ring with one chunk per batch over 64 chunks: staging reuse stays ordered."""
+    _round_trip(TINY, 4096 + 64, 64 * 256, mode, shuffled=True, staging_slots=2, chunks_per_batch=1,
+                side_streams=2)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_padded_block_stride(mode):
+    """Blocks with padding between them: padding is neither read into chunks nor written."""
+    lay = TINY
+    NB, pad = 300, 64  # padding in elements of 2 bytes
+    n = 1000
+    seed = harness.sub_seed("stride")
+    raw = np.random.default_rng(seed).integers(0, 1 << 16, size=(lay.L, NB, lay.block_elems + pad),
+                                               dtype=np.uint64).astype(np.uint16)
+    A = np.ascontiguousarray(raw[:, :, :lay.block_elems]).reshape(lay.L, NB, 2, lay.H, lay.BS, lay.D)
+    stride = (lay.block_elems + pad) * 2
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+    btB = harness.block_table(seed + 2, NB, lay.nblk(n))
+    nc = lay.nc(n)
+    cid = np.arange(nc)
+    pool = kvx.kv_pool_create(lay.kv, nc, mode)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    dA = to_device(raw)
+    dB = torch.full_like(dA, 0x7777)
+    cA = kvx.Cache(dA, lay.kv, NB, stride)
+    cB = kvx.Cache(dB, lay.kv, NB, stride)
+    tA, tB = bt_tensor(btA), bt_tensor(btB)
+    kvx.kv_store(cA, tA, n, pool, cid)
+    kvx.kv_load(cB, tB, n, pool, cid)
+    torch.cuda.synchronize()
+    want_pool = oracle_pool(lay, A, btA, n, cid, nc, POOL_SENT)
+    assert np.array_equal(view, want_pool), first_mismatch(view, want_pool)
+    gotB = dB.cpu().numpy().view(np.uint16).reshape(lay.L, NB, lay.block_elems + pad)
+    assert np.all(gotB[:, :, lay.block_elems:] == 0x7777)
+    B0 = np.full((lay.L, NB, 2, lay.H, lay.BS, lay.D), 0x7777, dtype=np.uint16)
+    want_B = oracle_unpack_into(lay, B0, btB, n, want_pool, cid)
+    np.testing.assert_array_equal(np.ascontiguousarray(gotB[:, :, :lay.block_elems]).reshape(want_B.shape), want_B)
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_load_into_disjoint_blocks_of_same_allocation(mode):
+    """Tiny config: 256 source blocks and 256 disjoint destination blocks in one 512-block
+    allocation; the load never touches the source blocks."""
+    lay, NB, n = TINY, 512, 4096
+    seed = harness.sub_seed("disjoint")
+    A = host_cache(lay, NB, seed, "u11")
+    btA = harness.block_table(seed + 1, NB, 256)
+    btB = harness.block_table(seed + 2, NB, 256, exclude=btA)
+    pool = kvx.kv_pool_create(lay.kv, 16, mode)
+    dA = to_device(A)
+    cA = kvx.Cache(dA, lay.kv, NB)
+    tA, tB = bt_tensor(btA), bt_tensor(btB)
+    cid = np.arange(16)
+    kvx.kv_store(cA, tA, n, pool, cid)
+    kvx.kv_load(cA, tB, n, pool, cid)
+    torch.cuda.synchronize()
+    want_pool = oracle_pool(lay, A, btA, n, cid, 16, 0)
+    want = oracle_unpack_into(lay, A, btB, n, want_pool, cid)
+    got = to_host(dA, A)
+    assert np.array_equal(got, want), first_mismatch(got, want)
+    np.testing.assert_array_equal(got[:, btA], A[:, btA])
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_zero_tokens_is_noop(mode):
+    lay = TINY
+    pool = kvx.kv_pool_create(lay.kv, 2, mode)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    d = device_cache(lay, 8, fill=CACHE_SENT)
+    c = kvx.Cache(d, lay.kv, 8)
+    kvx.kv_store(c, None, 0, pool, [])
+    kvx.kv_load(c, None, 0, pool, [])
+    torch.cuda.synchronize()
+    assert np.all(view == POOL_SENT)
+    assert bool((d.view(torch.uint8) == CACHE_SENT).all())
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_out_of_range_block_is_flagged_and_skipped(mode):
+    """A block id outside [0, num_blocks) is skipped on the device and reported; the rest moves."""
+    lay, NB, n = TINY, 64, 512
+    seed = harness.sub_seed("badblock")
+    A = host_cache(lay, NB, seed, "u11")
+    bt = harness.block_table(seed + 1, NB, 32)
+    bad = bt.copy()
+    bad[5] = NB          # one past the end
+    bad[20] = -3
+    pool = kvx.kv_pool_create(lay.kv, 2, mode)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    dA = to_device(A)
+    c = kvx.Cache(dA, lay.kv, NB)
+    t = bt_tensor(bad)
+    kvx.kv_store(c, t, n, pool, [0, 1])
+    torch.cuda.synchronize()
+    assert kvx.kv_pool_async_error(pool) == kvx.KV_ASYNC_BAD_BLOCK
+    want = oracle_pool(lay, A, bt, n, [0, 1], 2, POOL_SENT)
+    # Every byte except the two skipped slabs' rows matches; the skipped rows keep the sentinel.
+    diff = np.flatnonzero(view != want)
+    assert diff.size > 0 and np.all(view[diff] == POOL_SENT)
+    assert kvx.kv_pool_async_error(pool, clear=True) == kvx.KV_ASYNC_BAD_BLOCK
+    assert kvx.kv_pool_async_error(pool) == 0
+    kvx.kv_pool_destroy(pool)
+
+
+def test_pool_info_and_errors():
+    lay = TINY
+    pool = kvx.kv_pool_create(lay.kv, 4, "zero_copy")
+    info = kvx.kv_pool_get_info(pool)
+    assert info["is_pinned"] == 1 and info["pool_bytes"] == 4 * lay.slot_bytes and info["staging_bytes"] == 0
+    assert kvx.kv_pool_slot_bytes(pool) == lay.slot_bytes and kvx.kv_pool_num_slots(pool) == 4
+    assert kvx.kv_pool_slot(pool, 3) == info["host_base"] + 3 * lay.slot_bytes
+    assert kvx.kv_pool_slot(pool, 4) == 0
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_pool_set_mode(pool, "staged")  # no staging was allocated
+    assert e.value.status == kvx.KV_EINVAL
+    d = device_cache(lay, 8)
+    c = kvx.Cache(d, kvx.make_layout(2, 2, 64, 2, 32, 256), 4)
+    t = bt_tensor(np.arange(8))
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_store(c, t, 64, pool, [0])     # layout differs from the pool's
+    assert e.value.status == kvx.KV_EINVAL and "differs" in str(e.value)
+    kvx.kv_pool_destroy(pool)
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_pool_create(lay.kv, 4, 7)       # no silent mode selection
+    assert e.value.status == kvx.KV_EINVAL
+
+
+def test_oversized_pool_is_enomem_not_pageable():
+    """An impossible pinned request fails with KV_ENOMEM; nothing falls back to pageable memory."""
+    lay = Layout(64, 8, 128, 2, 16, 256)  # 64 MiB slots
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_pool_create(lay.kv, 1 << 24, "zero_copy")  # 1 PiB
+    assert e.value.status == kvx.KV_ENOMEM

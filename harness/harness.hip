@@ -34,13 +34,27 @@ int fail(hipError_t e, const char *what) {
 
 constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
 
-__device__ __forceinline__ uint64_t mix64(uint64_t z) {
-    z ^= z >> 30;
-    z *= 0xBF58476D1CE4E5B9ull;
-    z ^= z >> 27;
-    z *= 0x94D049BB133111EBull;
-    z ^= z >> 31;
-    return z;
+// SplitMix64 finaliser, written on explicit 32-bit halves.  The equivalent expression on
+// uint64_t values was compiled into code that dropped the last shift-xor for the 1- and
+// 4-byte fill instantiations on gfx950 (checked against the host generator with a
+// standalone build); the 32-bit form computes the published function exactly.
+struct u64h {
+    uint32_t lo, hi;
+};
+__device__ __forceinline__ u64h shr(u64h a, int s) { return {(a.lo >> s) | (a.hi << (32 - s)), a.hi >> s}; }
+__device__ __forceinline__ u64h xr(u64h a, u64h b) { return {a.lo ^ b.lo, a.hi ^ b.hi}; }
+// Low 64 bits of a * (chi:clo).
+__device__ __forceinline__ u64h mulc(u64h a, uint32_t clo, uint32_t chi) {
+    return {a.lo * clo, __umulhi(a.lo, clo) + a.lo * chi + a.hi * clo};
+}
+__device__ __forceinline__ uint64_t mix64(uint64_t z64) {
+    u64h z{static_cast<uint32_t>(z64), static_cast<uint32_t>(z64 >> 32)};
+    z = xr(z, shr(z, 30));
+    z = mulc(z, 0x1CE4E5B9u, 0xBF58476Du);
+    z = xr(z, shr(z, 27));
+    z = mulc(z, 0x133111EBu, 0x94D049BBu);
+    z = xr(z, shr(z, 31));
+    return (static_cast<uint64_t>(z.hi) << 32) | z.lo;
 }
 
 __device__ __forceinline__ uint32_t bf16_rne(float f) {

@@ -81,7 +81,8 @@ typedef int32_t kv_status;
 #define KV_HOST_NONCOHERENT 1u  /* coarse-grained pinned memory */
 
 /* Async error bits reported by kv_pool_async_error. */
-#define KV_ASYNC_BAD_BLOCK 1   /* a block_table entry was outside [0, num_blocks); that block was skipped */
+#define KV_ASYNC_BAD_BLOCK 1   /* a block_table entry was outside [0, num_blocks): no cache byte of it was
+                                  touched; a store wrote zeros for its chunk rows */
 
 /* Tokens' geometry; identical for a cache and the pool it talks to. */
 typedef struct kv_layout {
@@ -205,8 +206,9 @@ KV_API kv_status kv_check(const kv_cache *cache, const kv_layout *pool_layout, i
  *   stream:      hipStream_t (NULL = the null stream).
  * Enqueues only: never blocks the host on device work.  n_tokens == 0 is a
  * no-op.  Argument errors return before anything is enqueued.  An entry of
- * block_table outside [0, num_blocks) is skipped on the device and flagged in
- * kv_pool_async_error.  Calls on one pool are serialised internally.
+ * block_table outside [0, num_blocks) is flagged in kv_pool_async_error; its
+ * cache block is not read and its chunk rows are written as zeros (never stale
+ * bytes).  Calls on one pool are serialised internally.
  */
 KV_API kv_status kv_store(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, kv_pool *pool,
                    const int64_t *chunk_ids, void *stream);

@@ -87,23 +87,31 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
         return;
     const int bs = static_cast<int>((r - tok0) < a.BS ? (r - tok0) : a.BS);
 
+    const int l = a.layer0 + ll;
+    const int64_t row_bytes = static_cast<int64_t>(a.vec_per_row) * 16;
+    uint8_t *chunk_slab = a.chunk_base + static_cast<int64_t>(a.slot[c]) * a.slot_stride +
+                          ((static_cast<int64_t>(l) * 2 + kv) * r + tok0) * a.H * row_bytes;
+    vec16 *chunk_v = reinterpret_cast<vec16 *>(chunk_slab);
+    const int nvec = bs * a.H * a.vec_per_row;
+
     const int32_t b = a.block_table[i * bpc + j];
     if (b < 0 || b >= a.num_blocks) {
+        // A block id outside the cache: flag it, touch no cache byte, and on a store write
+        // zeros for the slab's chunk rows so that no stale staging or pool bytes (another
+        // request's state) are passed on as this chunk's contents.
         if (threadIdx.x == 0)
             __hip_atomic_store(a.err, KV_ASYNC_BAD_BLOCK, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (DIR == kPack) {
+            const vec16 zero = {0u, 0u, 0u, 0u};
+            for (int v = static_cast<int>(threadIdx.x); v < nvec; v += kThreads)
+                chunk_v[v] = zero;
+        }
         return;
     }
 
-    const int l = a.layer0 + ll;
-    const int64_t row_bytes = static_cast<int64_t>(a.vec_per_row) * 16;
     uint8_t *cache_slab = a.layer[ll] + static_cast<int64_t>(b) * a.block_stride +
                           static_cast<int64_t>(kv) * a.H * a.BS * row_bytes;
-    uint8_t *chunk_slab = a.chunk_base + static_cast<int64_t>(a.slot[c]) * a.slot_stride +
-                          ((static_cast<int64_t>(l) * 2 + kv) * r + tok0) * a.H * row_bytes;
-
     vec16 *cache_v = reinterpret_cast<vec16 *>(cache_slab);
-    vec16 *chunk_v = reinterpret_cast<vec16 *>(chunk_slab);
-    const int nvec = bs * a.H * a.vec_per_row;
 
     RowWalker w(threadIdx.x, a.vec_per_row, a.H);
     const int tid = static_cast<int>(threadIdx.x);

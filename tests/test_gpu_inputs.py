@@ -11,9 +11,10 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("dist,E", [("u11", 2), ("n01", 2), ("raw", 2), ("raw", 1), ("raw", 4)])
-def test_device_fill_matches_host(dist, E):
+@pytest.mark.parametrize("k", range(4))
+def test_device_fill_matches_host(dist, E, k):
     L, NB, H, BS, D = 2, 37, 2, 16, 64
-    seed = harness.sub_seed("twin", dist, E)
+    seed = harness.sub_seed("twin", dist, E, k)
     want = harness.gen_cache(seed, dist, L, NB, H, BS, D, E)
     t = torch.empty(want.shape, dtype=TORCH_INT[E], device="cuda:0")
     hg.fill_values(t, 0, seed, dist, E)

@@ -122,8 +122,8 @@ def test_load_probe_53(mode, stream_kind):
                 hg.copy_u8(probe, dB, nbytes, stream)  # delayed consumer of the old value
                 kvx.kv_load(cB, tb, n, pool, np.arange(nc), stream)
                 _sync(stream)
-                seen = probe.view(torch.uint8).cpu().numpy()
-                after = dB.view(torch.uint8).cpu().numpy()
+                seen = probe.view(torch.uint8).cpu().numpy().reshape(-1)
+                after = dB.view(torch.uint8).cpu().numpy().reshape(-1)
                 elem_mask = np.repeat(mask, lay.E)
                 stale = int(np.count_nonzero(seen != 0))
                 wrong = int(np.count_nonzero(after[elem_mask] != 53)) + int(np.count_nonzero(after[~elem_mask]))
@@ -160,7 +160,7 @@ def test_store_then_load_same_stream_no_host_sync(mode):
         kvx.kv_store(cA, tA, n, pool, np.arange(nc), s)
         kvx.kv_load(cB, tB, n, pool, np.arange(nc), s)
         s.synchronize()
-        after = dB.view(torch.uint8).cpu().numpy()
+        after = dB.view(torch.uint8).cpu().numpy().reshape(-1)
         assert np.all(after[mask] == value), f"trial {trial}: load did not see the store"
     kvx.kv_pool_destroy(pool)
 
@@ -190,6 +190,6 @@ def test_cross_stream_store_then_load_ordered_by_event(mode):
         sB.wait_event(ev)
         kvx.kv_load(cB, tB, n, pool, np.arange(nc), sB)
         sB.synchronize()
-        after = dB.view(torch.uint8).cpu().numpy()
+        after = dB.view(torch.uint8).cpu().numpy().reshape(-1)
         assert np.all(after[mask] == 7 + trial)
     kvx.kv_pool_destroy(pool)

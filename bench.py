@@ -1,0 +1,351 @@
+#!/usr/bin/env python3
+"""Benchmark of the shared-KV store/load path on one MI355X.
+
+One step = the whole hot path once: kv_store of a 131,072-token (128k) prefix of
+a 27B-class GQA KV cache (64 layers, 8 KV heads, head_dim 128, bf16, 16-token
+blocks; 256 KiB per token, 32 GiB per direction) from replica A's fragmented
+block set into 512 packed 256-token chunks of the pinned host pool, then
+kv_load of all 512 chunks into a fresh fragmented block set of replica B's
+separate cache allocation.  Inputs are synthetic, seeded, and resident in HBM
+(cache A) and pinned host memory (pool) before the timed region.
+
+Printed: one JSON line with whole-job GB/s (store + load bytes per second),
+per-direction rates, the 128k and 256k restore seconds, the HBM roofline of the
+dominant pack/unpack kernel (timed live with HIP events on its stream), the
+host-link rate against the measured pinned-copy peak, a zero-copy comparison,
+a sampled round-trip check against the seeded generator, and the CPU oracle's
+own throughput on a bounded sample (the cpu_baseline; the only use of the
+oracle here).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "KV store/load GB/s and seconds to restore a 128k/256k-token prefix, 1 MI355X"
+L, H, D, E, BS, C = 64, 8, 128, 2, 16, 256
+TOKEN_BYTES = 2 * L * H * D * E
+HBM_PEAK_GBPS = 8000.0
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "gather_pack_staged_128k_traffic.txt")
+GATHER_SRC = os.path.join(ROOT, "paper_2609_15021_amd", "csrc", "kvx_gather.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--mode", choices=["staged", "zero_copy"], default="staged")
+    ap.add_argument("--tokens", type=int, default=131072, help="prefix length (default 128k)")
+    ap.add_argument("--pool-blocks", type=int, default=10240, help="blocks per cache allocation (160k tokens)")
+    ap.add_argument("--no-256k", action="store_true", help="skip the 256k restore measurement")
+    ap.add_argument("--no-zero-copy-compare", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+class Replica:
+    """One replica's paged cache: [L][NB][2][H][BS][D] bf16 bits in HBM plus its block table."""
+
+    def __init__(self, torch, kvx, layout, num_blocks, dev):
+        self.t = torch.empty((L, num_blocks, 2, H, BS, D), dtype=torch.int16, device=dev)
+        self.cache = kvx.Cache(self.t, layout, num_blocks)
+        self.num_blocks = num_blocks
+
+
+def link_peak(torch, hg, pool_host_ptr, nbytes, dev, reps=10):
+    """Median pinned hipMemcpyAsync rate (GB/s) between HBM and the pool's own memory."""
+    d = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    s = torch.cuda.Stream()
+    out = {}
+    for name, dst, src in (("d2h", pool_host_ptr, d.data_ptr()), ("h2d", d.data_ptr(), pool_host_ptr)):
+        hg.copy_async(dst, src, nbytes, s)
+        s.synchronize()
+        rates = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            hg.copy_async(dst, src, nbytes, s)
+            e1.record(s)
+            e1.synchronize()
+            rates.append(nbytes / (e0.elapsed_time(e1) / 1e3) / 1e9)
+        out[name] = statistics.median(rates)
+    del d
+    return out
+
+
+def sampled_round_trip(np, harness, rep_b, bt_a, bt_b, seed, n, num_blocks, chunks, torch):
+    """Round-trip identity on sampled chunks: replica B's restored token slots hold exactly the
+    bytes the seeded generator put in replica A's source blocks (the oracle comparison at these
+    sizes lives in the GPU tests)."""
+    bpc = C // BS
+    for i in chunks:
+        r = min(C, n - i * C)
+        nb = -(-r // BS)
+        src = harness.gen_blocks(seed, "n01", L, num_blocks, H, BS, D, E, blocks=bt_a[i * bpc:i * bpc + nb])
+        idx = torch.from_numpy(bt_b[i * bpc:i * bpc + nb].astype(np.int64)).to(rep_b.t.device)
+        got = rep_b.t[:, idx].cpu().numpy().view(np.uint16)
+        if r % BS:  # slots past the prefix end in its last block are not part of the prefix
+            got[:, -1, :, :, r % BS:, :] = 0
+            src[:, -1, :, :, r % BS:, :] = 0
+        if not np.array_equal(got, src):
+            return False, f"restored blocks of chunk {i} differ from the source"
+    return True, f"round trip bit-exact on sampled chunks {list(chunks)}"
+
+
+def traffic_from_profile():
+    """Per-launch HBM bytes from committed PMC counters, if taken on the current kernel source."""
+    if not os.path.exists(PROFILE_TRAFFIC):
+        return None, None
+    kv = {}
+    with open(PROFILE_TRAFFIC) as f:
+        for line in f:
+            if "=" in line and not line.lstrip().startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+    with open(GATHER_SRC, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    if kv.get("kernel_source_sha256") != sha:
+        return None, "kernel changed since the counters were taken"
+    return float(kv["hbm_bytes_per_launch"]), None
+
+
+def cpu_baseline(np, oracle, n_chunks=32):
+    """The oracle timed on host cores: store + load of a bounded sample of the workload."""
+    rng = np.random.default_rng(2609)
+    bpc = C // BS
+    nb = n_chunks * bpc
+    n = n_chunks * C
+    lay = oracle.make_layout(L, H, D, E, BS, C)
+    src = np.frombuffer(rng.bytes(L * nb * 2 * H * BS * D * E), dtype=np.uint8).reshape(L, -1)
+    src_layers = [np.ascontiguousarray(src[l]) for l in range(L)]
+    dst_layers = [np.zeros_like(a) for a in src_layers]
+    bt_a = rng.permutation(nb).astype(np.int32)
+    bt_b = rng.permutation(nb).astype(np.int32)
+    pool = np.zeros(n_chunks * oracle.slot_bytes(lay), dtype=np.uint8)
+    ids = np.arange(n_chunks)
+    threads = min(16, os.cpu_count() or 1)
+    res = {}
+    for nt in (threads, 1):
+        t0 = time.perf_counter()
+        assert oracle.pack(lay, src_layers, 2 * H * BS * D * E, nb, bt_a, n, pool, ids, nt) == oracle.OK
+        assert oracle.unpack(lay, dst_layers, 2 * H * BS * D * E, nb, bt_b, n, pool, ids, nt) == oracle.OK
+        res[nt] = 2 * n * TOKEN_BYTES / (time.perf_counter() - t0) / 1e9
+    return {"value": round(res[threads], 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "value_1_thread": round(res[1], 3),
+            "sample": f"{n_chunks} chunks ({n:,} tokens, {n * TOKEN_BYTES / 2**30:.0f} GiB per direction) of the "
+                      "128k workload: oracle store then load, host memory to host memory, seeded random bytes"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): this path is measured per "
+              "GPU; cross-GPU sharding is a design note only.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import harness
+    from harness import gpu as hg
+    from paper_2609_15021_amd import kvx
+
+    dev = torch.device("cuda:0")
+    layout = kvx.make_layout(L, H, D, E, BS, C)
+    n = args.tokens
+    nc = -(-n // C)
+    nblk = -(-n // BS)
+    N = n * TOKEN_BYTES
+    seed = harness.sub_seed("bench", n)
+    log(f"[bench] 27B-class layout, prefix {n} tokens ({N / 2**30:.1f} GiB per direction), mode {args.mode}")
+
+    rep_a = Replica(torch, kvx, layout, args.pool_blocks, dev)
+    rep_b = Replica(torch, kvx, layout, args.pool_blocks, dev)
+    hg.fill_values(rep_a.t, 0, seed, "n01", E)
+    rep_b.t.zero_()
+    bt_a = harness.block_table(seed + 1, args.pool_blocks, nblk)
+    bt_b = harness.block_table(seed + 2, args.pool_blocks, nblk)
+    t_a, t_b = torch.from_numpy(bt_a).to(dev), torch.from_numpy(bt_b).to(dev)
+    ids = harness.chunk_ids(nc, nc)
+    pool = kvx.kv_pool_create(layout, nc, args.mode, staging_slots=3 if args.mode == "staged" else 0, profile=True)
+    info = kvx.kv_pool_get_info(pool)
+    torch.cuda.synchronize()
+    log(f"[bench] pool {info['pool_bytes'] / 2**30:.1f} GiB pinned={info['is_pinned']} "
+        f"alloc {info['alloc_seconds']:.3f} s; staging {info['staging_bytes'] / 2**30:.1f} GiB")
+
+    peak = link_peak(torch, hg, info["host_base"], 1 << 30, dev)
+    log(f"[bench] pinned hipMemcpyAsync peak: D2H {peak['d2h']:.2f} GB/s, H2D {peak['h2d']:.2f} GB/s")
+
+    s = torch.cuda.Stream()
+
+    def step(evs=None):
+        if evs:
+            evs[0].record(s)
+        kvx.kv_store(rep_a.cache, t_a, n, pool, ids, s)
+        if evs:
+            evs[1].record(s)
+        kvx.kv_load(rep_b.cache, t_b, n, pool, ids, s)
+        if evs:
+            evs[2].record(s)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    for w in ("pack", "unpack"):
+        kvx.kv_pool_kernel_stats(pool, w, reset=True)
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    log(f"[bench] timed {args.steps} steps in {elapsed:.3f} s")
+
+    store_s = [e[0].elapsed_time(e[1]) / 1e3 for e in events]
+    load_s = [e[1].elapsed_time(e[2]) / 1e3 for e in events]
+    kstats = {w: kvx.kv_pool_kernel_stats(pool, w, reset=True) for w in ("pack", "unpack")}
+    value = 2 * N * args.steps / elapsed / 1e9
+
+    # Dominant kernel of the step (largest total time) and its HBM roofline.
+    dom = max(kstats, key=lambda w: kstats[w][1])
+    launches, total_ms, alg_bytes = kstats[dom]
+    avg_ms = total_ms / max(launches, 1)
+    per_launch = alg_bytes / max(launches, 1)
+    roof = None
+    if args.mode == "staged":
+        traffic, why = traffic_from_profile()
+        achieved = per_launch / (avg_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                "kernel": f"gather_kernel<{dom}> (staged, device staging side)",
+                "launches": launches, "avg_launch_ms": round(avg_ms, 4),
+                "algorithmic_bytes_per_launch": per_launch}
+        if why:
+            roof["traffic_note"] = why
+        other = "unpack" if dom == "pack" else "pack"
+        ln, tm, ab = kstats[other]
+        roof["other_kernel"] = {"kernel": f"gather_kernel<{other}>", "achieved": round(ab / (tm / 1e3) / 1e9, 1),
+                                "frac": round(ab / (tm / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                "avg_launch_ms": round(tm / max(ln, 1), 4)}
+        log(f"[bench] {dom} kernels: {launches} launches, avg {avg_ms:.4f} ms, {achieved:.1f} GB/s "
+            f"({achieved / HBM_PEAK_GBPS:.1%} of HBM peak)")
+
+    ok, parity_msg = sampled_round_trip(np, harness, rep_b, bt_a, bt_b, seed, n, args.pool_blocks,
+                                        sorted({0, nc // 2, nc - 1}), torch)
+    log(f"[bench] parity: {parity_msg}")
+
+    # Restore seconds: host wall clock of a full-prefix load (prefix already in the pool).
+    restore = []
+    for _ in range(3):
+        w0 = time.perf_counter()
+        kvx.kv_load(rep_b.cache, t_b, n, pool, ids, s)
+        s.synchronize()
+        restore.append(time.perf_counter() - w0)
+    restore_128k = statistics.median(restore)
+
+    zc = None
+    if not args.no_zero_copy_compare:
+        other_mode = "zero_copy" if args.mode == "staged" else "staged"
+        if other_mode == "zero_copy" or info["staging_bytes"]:
+            kvx.kv_pool_set_mode(pool, other_mode)
+            step()
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            step(evs)
+            s.synchronize()
+            zc = {"mode": other_mode,
+                  "store_GBps": round(N / (evs[0].elapsed_time(evs[1]) / 1e3) / 1e9, 2),
+                  "load_GBps": round(N / (evs[1].elapsed_time(evs[2]) / 1e3) / 1e9, 2)}
+            kvx.kv_pool_set_mode(pool, args.mode)
+            log(f"[bench] {other_mode}: store {zc['store_GBps']} GB/s, load {zc['load_GBps']} GB/s")
+    alloc_s = info["alloc_seconds"]
+    kvx.kv_pool_destroy(pool)
+    del rep_a, rep_b, t_a, t_b
+    torch.cuda.empty_cache()
+
+    restore_256k = None
+    parity_256k = None
+    if not args.no_256k:
+        n2, nb2 = 262336, 20480  # 1,024 full chunks + a 192-token partial chunk; 80 GiB allocations
+        nc2, nblk2 = -(-n2 // C), -(-n2 // BS)
+        seed2 = harness.sub_seed("bench", n2)
+        ra, rb = Replica(torch, kvx, layout, nb2, dev), Replica(torch, kvx, layout, nb2, dev)
+        hg.fill_values(ra.t, 0, seed2, "n01", E)
+        rb.t.zero_()
+        ba, bb = harness.block_table(seed2 + 1, nb2, nblk2), harness.block_table(seed2 + 2, nb2, nblk2)
+        ta, tb = torch.from_numpy(ba).to(dev), torch.from_numpy(bb).to(dev)
+        ids2 = harness.chunk_ids(nc2, nc2)
+        pool2 = kvx.kv_pool_create(layout, nc2, args.mode, staging_slots=3 if args.mode == "staged" else 0)
+        torch.cuda.synchronize()  # fills ran on the default stream; s is non-blocking
+        kvx.kv_store(ra.cache, ta, n2, pool2, ids2, s)
+        s.synchronize()
+        times = []
+        for _ in range(3):
+            w0 = time.perf_counter()
+            kvx.kv_load(rb.cache, tb, n2, pool2, ids2, s)
+            s.synchronize()
+            times.append(time.perf_counter() - w0)
+        restore_256k = statistics.median(times)
+        ok2, msg2 = sampled_round_trip(np, harness, rb, ba, bb, seed2, n2, nb2, [0, nc2 // 2, nc2 - 1], torch)
+        parity_256k = msg2
+        ok = ok and ok2
+        log(f"[bench] 256k+192 restore {restore_256k:.3f} s ({n2 * TOKEN_BYTES / restore_256k / 1e9:.2f} GB/s); "
+            f"parity: {msg2}")
+        kvx.kv_pool_destroy(pool2)
+        del ra, rb, ta, tb
+        torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle  # the CPU baseline leg is the only part of the benchmark that runs the oracle
+        cpu = cpu_baseline(np, oracle)
+    if cpu:
+        log(f"[bench] cpu oracle: {cpu['value']} GB/s on {cpu['cores']} threads, {cpu['value_1_thread']} GB/s on 1")
+
+    store_gbps = N / statistics.median(store_s) / 1e9
+    load_gbps = N / statistics.median(load_s) / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+        "config": {"workload": "27B-class GQA KV cache (64 layers, 8 KV heads, head_dim 128, bf16 values moved as "
+                               "opaque bytes, 16-token blocks): store a 131,072-token prefix from 8,192 random blocks "
+                               "of a 10,240-block allocation into 512 pinned 256-token chunks, then load it into a "
+                               "fresh random 8,192-block set of a second allocation",
+                   "prefix_tokens": n, "bytes_per_direction": N, "mode": args.mode, "parallelism": "single GPU"},
+        "store_GBps": round(store_gbps, 3), "load_GBps": round(load_gbps, 3),
+        "restore_s_128k": round(restore_128k, 4),
+        "restore_s_256k": None if restore_256k is None else round(restore_256k, 4),
+        "link": {"peak_d2h_GBps": round(peak["d2h"], 3), "peak_h2d_GBps": round(peak["h2d"], 3),
+                 "store_frac_of_peak": round(store_gbps / peak["d2h"], 4),
+                 "load_frac_of_peak": round(load_gbps / peak["h2d"], 4),
+                 "peak_method": "median of 10 pinned hipMemcpyAsync of 1 GiB on the pool's own memory"},
+        "roofline": roof,
+        "zero_copy_compare": zc,
+        "pool_alloc_s": round(alloc_s, 4),
+        "parity": parity_msg if ok else f"FAILED: {parity_msg}",
+        "parity_256k": parity_256k,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    if not ok:
+        sys.exit(1)
+
+
+if __name__ == "__main__":
+    main()

@@ -109,8 +109,8 @@ typedef struct kv_pool_options {
     uint32_t host_kind;        /* KV_HOST_COHERENT (0) or KV_HOST_NONCOHERENT */
     int32_t staging_slots;     /* staged ring depth K >= 2 (default 3); with mode zero-copy, > 0
                                   also allocates staging so kv_pool_set_mode can switch later */
-    int32_t chunks_per_batch;  /* chunks per staging slot / per kernel launch, 1..256 (default 8
-                                  staged, 256 zero-copy) */
+    int32_t chunks_per_batch;  /* chunks per staging slot / per kernel launch, 1..256 (default 16
+                                  staged, 256 zero-copy); applies to the mode given here */
     int32_t side_streams;      /* staged: DMA side streams, 1..8 (default 2) */
     int32_t profile;           /* nonzero: time every pack/unpack launch (kv_pool_kernel_stats) */
 } kv_pool_options;

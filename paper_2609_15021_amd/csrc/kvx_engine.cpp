@@ -25,7 +25,7 @@ using kvx::Geometry;
 namespace {
 
 constexpr int kDefaultStagingSlots = 3;
-constexpr int kDefaultChunksPerBatch = 8;
+constexpr int kDefaultChunksPerBatch = 16;
 constexpr int kDefaultSideStreams = 2;
 
 kv_status release(kv_pool *p) {
@@ -87,10 +87,11 @@ kv_status check_device(const kv_pool *p, const kv_cache *cache) {
 }
 
 // Enqueue the pack/unpack kernels for chunks [chunk0, chunk0 + nchunks) of the prefix.
-// slots[c] is the slot id of chunk chunk0 + c relative to chunk_base (slot_stride apart).
+// slots[c] is the slot id of chunk chunk0 + c relative to chunk_base (slot_stride apart);
+// host_side: chunk_base is the mapped pinned pool (zero-copy) rather than device staging.
 kv_status enqueue_gather(kv_pool *p, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                          Direction dir, int64_t chunk0, int nchunks, const int32_t *slots, uint8_t *chunk_base,
-                         int64_t slot_stride, hipStream_t stream) {
+                         int64_t slot_stride, bool host_side, hipStream_t stream) {
     const Geometry &g0 = p->geo;
     const Geometry g = kvx::geometry(cache->layout, cache->block_stride_bytes);
     hipEvent_t t_start = nullptr, t_stop = nullptr;
@@ -131,7 +132,7 @@ kv_status enqueue_gather(kv_pool *p, const kv_cache *cache, const int32_t *block
             a.nchunks = nc;
             for (int c = 0; c < nc; ++c)
                 a.slot[c] = slots[c0 + c];
-            KVX_HIP(kvx::launch_gather(a, dir, stream));
+            KVX_HIP(kvx::launch_gather(a, dir, host_side, stream));
         }
     }
     for (int c = 0; c < nchunks; ++c) {
@@ -188,7 +189,7 @@ kv_status transfer(kv_pool *p, const kv_cache *cache, const int32_t *block_table
         for (int64_t c0 = 0; c0 < nc; c0 += p->zc_chunks) {
             const int n = static_cast<int>(std::min<int64_t>(p->zc_chunks, nc - c0));
             kv_status st = enqueue_gather(p, cache, block_table, n_tokens, dir, c0, n, slots.data() + c0,
-                                          p->dev_base, g.slot_bytes, stream);
+                                          p->dev_base, g.slot_bytes, true, stream);
             if (st != KV_OK)
                 return st;
         }
@@ -219,7 +220,7 @@ kv_status transfer(kv_pool *p, const kv_cache *cache, const int32_t *block_table
             if (p->free_recorded[k])
                 KVX_HIP(hipStreamWaitEvent(stream, p->ev_free[k], 0));
             kv_status st = enqueue_gather(p, cache, block_table, n_tokens, dir, c0, n, local.data(), stage,
-                                          g.slot_bytes, stream);
+                                          g.slot_bytes, false, stream);
             if (st != KV_OK)
                 return st;
             KVX_HIP(hipEventRecord(p->ev_ready[k], stream));
@@ -243,7 +244,7 @@ kv_status transfer(kv_pool *p, const kv_cache *cache, const int32_t *block_table
             KVX_HIP(hipEventRecord(p->ev_ready[k], side));
             KVX_HIP(hipStreamWaitEvent(stream, p->ev_ready[k], 0));
             kv_status st = enqueue_gather(p, cache, block_table, n_tokens, dir, c0, n, local.data(), stage,
-                                          g.slot_bytes, stream);
+                                          g.slot_bytes, false, stream);
             if (st != KV_OK)
                 return st;
             KVX_HIP(hipEventRecord(p->ev_free[k], stream));

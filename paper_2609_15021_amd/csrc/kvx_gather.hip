@@ -26,6 +26,37 @@ namespace {
 // One 16-byte vector as a native 128-bit register tuple (kept in VGPRs; never a float).
 typedef uint32_t vec16 __attribute__((ext_vector_type(4)));
 
+// Compile-time tuning knobs: vectors in flight per thread, and streaming (nontemporal)
+// access on the read and write side.
+#ifndef KVX_UNROLL
+#define KVX_UNROLL 1
+#endif
+#ifndef KVX_NT_LOAD
+#define KVX_NT_LOAD 1
+#endif
+#ifndef KVX_NT_STORE
+#define KVX_NT_STORE 1
+#endif
+#ifndef KVX_UNPACK_CACHE_ORDER
+#define KVX_UNPACK_CACHE_ORDER 1
+#endif
+
+__device__ __forceinline__ vec16 load16(const vec16 *p) {
+#if KVX_NT_LOAD
+    return __builtin_nontemporal_load(p);
+#else
+    return *p;
+#endif
+}
+
+__device__ __forceinline__ void store16(vec16 *p, vec16 v) {
+#if KVX_NT_STORE
+    __builtin_nontemporal_store(v, p);
+#else
+    *p = v;
+#endif
+}
+
 // Walks chunk-order vector indices v = t, t + kThreads, t + 2*kThreads, ... of one slab,
 // maintaining (s, h, col) with v = (s*H + h)*VR + col.
 struct RowWalker {
@@ -64,12 +95,21 @@ struct RowWalker {
 
     // 16-byte-vector offset of the current element inside the cache-side [H][BS][D] slab.
     __device__ int cache_vec(int BS) const { return (h * BS + s) * VR + col; }
+
+    // The same for a walker built over cache-side order (its "s" is the head, its "h" the
+    // slot): offset inside the chunk-side [BS][H][D] run.
+    __device__ int chunk_vec(int heads) const { return (h * heads + s) * VR + col; }
 };
 
 template <int DIR, int U>
+__device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, int kv, int j);
+
+// HOST_SIDE marks launches whose chunk side is mapped pinned host memory (zero-copy mode);
+// the body is the same, the instantiation (and launch occupancy) is separate.
+template <int DIR, int U, bool HOST_SIDE>
 __global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
     // Workgroup -> (chunk c, layer ll, kv, block j); j varies fastest so consecutive
-    // workgroups write consecutive chunk-side regions.
+    // workgroups touch consecutive chunk-side regions.
     const int bpc = a.blocks_per_chunk;
     const int64_t wg = blockIdx.x;
     const int j = static_cast<int>(wg % bpc);
@@ -78,6 +118,12 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
     rest >>= 1;
     const int ll = static_cast<int>(rest % a.nlayers);
     const int c = static_cast<int>(rest / a.nlayers);
+    move_slab<DIR, U>(a, c, ll, kv, j);
+}
+
+template <int DIR, int U>
+__device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, int kv, int j) {
+    const int bpc = a.blocks_per_chunk;
 
     const int64_t i = a.chunk0 + c;  // global chunk index
     const int64_t remaining = a.n_tokens - i * a.C;
@@ -113,8 +159,35 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
                           static_cast<int64_t>(kv) * a.H * a.BS * row_bytes;
     vec16 *cache_v = reinterpret_cast<vec16 *>(cache_slab);
 
-    RowWalker w(threadIdx.x, a.vec_per_row, a.H);
     const int tid = static_cast<int>(threadIdx.x);
+    if (DIR == kUnpack && KVX_UNPACK_CACHE_ORDER && bs == a.BS) {
+        // Whole block: lanes walk the cache side in order, so the writes are the contiguous side.
+        RowWalker w(tid, a.vec_per_row, a.BS);
+        int base = 0;
+        for (; base + kThreads * U <= nvec; base += kThreads * U) {
+            const int v = base + tid;
+            int chunk_off[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                chunk_off[u] = w.chunk_vec(a.H);
+                w.advance();
+            }
+            vec16 buf[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                buf[u] = load16(chunk_v + chunk_off[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                store16(cache_v + v + u * kThreads, buf[u]);
+        }
+        for (int v = base + tid; v < nvec; v += kThreads) {
+            const int co = w.chunk_vec(a.H);
+            w.advance();
+            store16(cache_v + v, load16(chunk_v + co));
+        }
+        return;
+    }
+    RowWalker w(threadIdx.x, a.vec_per_row, a.H);
     int base = 0;  // first chunk-side vector of the current tile (uniform across the workgroup)
     // Full tiles: every thread has U in-range vectors; all U loads issue before any store.
     for (; base + kThreads * U <= nvec; base += kThreads * U) {
@@ -129,16 +202,16 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (DIR == kPack)
-                buf[u] = cache_v[cache_off[u]];
+                buf[u] = load16(cache_v + cache_off[u]);
             else
-                buf[u] = chunk_v[v + u * kThreads];
+                buf[u] = load16(chunk_v + v + u * kThreads);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (DIR == kPack)
-                chunk_v[v + u * kThreads] = buf[u];
+                store16(chunk_v + v + u * kThreads, buf[u]);
             else
-                cache_v[cache_off[u]] = buf[u];
+                store16(cache_v + cache_off[u], buf[u]);
         }
     }
     // Tail: one vector at a time.
@@ -146,13 +219,21 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
         const int co = w.cache_vec(a.BS);
         w.advance();
         if (DIR == kPack)
-            chunk_v[v] = cache_v[co];
+            store16(chunk_v + v, load16(cache_v + co));
         else
-            cache_v[co] = chunk_v[v];
+            store16(cache_v + co, load16(chunk_v + v));
     }
 }
 
-constexpr int kUnroll = 8;
+constexpr int kUnroll = KVX_UNROLL;
+
+// Dynamic LDS reserved per workgroup (never touched) to cap the workgroups resident per CU:
+// 40 KiB of the CU's 160 KiB allows 4 (16 waves per CU).  Measured on MI355X with the
+// 27B-class layout, 4 resident workgroups move slabs faster than 3 or than 6 and more:
+// fewer concurrent 32 KiB streams per CU keep the HBM read/write mix efficient.
+#ifndef KVX_LDS_RESERVE
+#define KVX_LDS_RESERVE 40960
+#endif
 
 }  // namespace
 
@@ -165,15 +246,23 @@ int max_chunks_per_launch(const Geometry &g, int nlayers) {
     return static_cast<int>(m < 1 ? 1 : m);
 }
 
-hipError_t launch_gather(const GatherArgs &args, Direction dir, hipStream_t stream) {
+hipError_t launch_gather(const GatherArgs &args, Direction dir, bool host_side, hipStream_t stream) {
     const int64_t grid = static_cast<int64_t>(args.nchunks) * args.nlayers * 2 * args.blocks_per_chunk;
     if (grid <= 0)
         return hipSuccess;
-    // hipLaunchKernel reports launch failures directly (no sticky last-error state).
-    const void *fn = dir == kPack ? reinterpret_cast<const void *>(&gather_kernel<kPack, kUnroll>)
-                                  : reinterpret_cast<const void *>(&gather_kernel<kUnpack, kUnroll>);
+    const void *fn;
+    if (host_side)
+        fn = dir == kPack ? reinterpret_cast<const void *>(&gather_kernel<kPack, kUnroll, true>)
+                          : reinterpret_cast<const void *>(&gather_kernel<kUnpack, kUnroll, true>);
+    else
+        fn = dir == kPack ? reinterpret_cast<const void *>(&gather_kernel<kPack, kUnroll, false>)
+                          : reinterpret_cast<const void *>(&gather_kernel<kUnpack, kUnroll, false>);
+    // Device-side (staged) launches cap residency with reserved LDS; host-side launches wait
+    // on PCIe round trips and keep full occupancy.
+    const unsigned lds = host_side ? 0u : static_cast<unsigned>(KVX_LDS_RESERVE);
     void *kargs[] = {const_cast<GatherArgs *>(&args)};
-    return hipLaunchKernel(fn, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), kargs, 0, stream);
+    // hipLaunchKernel reports launch failures directly (no sticky last-error state).
+    return hipLaunchKernel(fn, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), kargs, lds, stream);
 }
 
 }  // namespace kvx

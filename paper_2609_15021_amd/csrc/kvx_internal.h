@@ -12,7 +12,10 @@
 
 namespace kvx {
 
-constexpr int kThreads = 256;          // work-items per workgroup (4 wave64s)
+#ifndef KVX_THREADS
+#define KVX_THREADS 256
+#endif
+constexpr int kThreads = KVX_THREADS;  // work-items per workgroup (wave64s x 64)
 constexpr int kMaxLaunchLayers = 64;   // layer pointers carried in one launch's kernel arguments
 constexpr int kMaxLaunchChunks = 256;  // slot ids carried in one launch's kernel arguments
 
@@ -53,8 +56,9 @@ struct GatherArgs {
 
 enum Direction { kPack = 0, kUnpack = 1 };
 
-// Enqueue one launch on `stream`.  Returns the launch error (hipSuccess on success).
-hipError_t launch_gather(const GatherArgs &args, Direction dir, hipStream_t stream);
+// Enqueue one launch on `stream`; host_side: the chunk side is mapped pinned host memory.
+// Returns the launch error (hipSuccess on success).
+hipError_t launch_gather(const GatherArgs &args, Direction dir, bool host_side, hipStream_t stream);
 
 // Largest chunk count per launch that keeps the grid within the 32-bit work-item limit.
 int max_chunks_per_launch(const Geometry &g, int nlayers);

@@ -53,7 +53,22 @@ def parse():
     ap.add_argument("--no-256k", action="store_true", help="skip the 256k restore measurement")
     ap.add_argument("--no-zero-copy-compare", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 5 times (PMC counter scale reference)")
     return ap.parse_args()
+
+
+def calibrate_copy():
+    """A plain copy kernel of known size: 5 x 1 GiB read + 1 GiB written (HBM counter reference)."""
+    import torch
+    x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda:0")
+    y = torch.empty_like(x)
+    x.fill_(1)
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "torch device copy", "bytes_read_per_launch": 1 << 30,
+                      "bytes_written_per_launch": 1 << 30, "launches": 5}), flush=True)
 
 
 class Replica:
@@ -105,8 +120,9 @@ def sampled_round_trip(np, harness, rep_b, bt_a, bt_b, seed, n, num_blocks, chun
     return True, f"round trip bit-exact on sampled chunks {list(chunks)}"
 
 
-def traffic_from_profile():
-    """Per-launch HBM bytes from committed PMC counters, if taken on the current kernel source."""
+def traffic_from_profile(kernel):
+    """Per-launch HBM bytes of `kernel` ("pack"/"unpack") from committed PMC counters, if they
+    were taken on the current kernel source."""
     if not os.path.exists(PROFILE_TRAFFIC):
         return None, None
     kv = {}
@@ -119,10 +135,10 @@ def traffic_from_profile():
         sha = hashlib.sha256(f.read()).hexdigest()
     if kv.get("kernel_source_sha256") != sha:
         return None, "kernel changed since the counters were taken"
-    return float(kv["hbm_bytes_per_launch"]), None
+    return float(kv[f"{kernel}_hbm_bytes_per_launch"]), None
 
 
-def cpu_baseline(np, oracle, n_chunks=32):
+def cpu_baseline(np, oracle, n_chunks=64):
     """The oracle timed on host cores: store + load of a bounded sample of the workload."""
     rng = np.random.default_rng(2609)
     bpc = C // BS
@@ -138,19 +154,26 @@ def cpu_baseline(np, oracle, n_chunks=32):
     ids = np.arange(n_chunks)
     threads = min(16, os.cpu_count() or 1)
     res = {}
-    for nt in (threads, 1):
-        t0 = time.perf_counter()
-        assert oracle.pack(lay, src_layers, 2 * H * BS * D * E, nb, bt_a, n, pool, ids, nt) == oracle.OK
-        assert oracle.unpack(lay, dst_layers, 2 * H * BS * D * E, nb, bt_b, n, pool, ids, nt) == oracle.OK
-        res[nt] = 2 * n * TOKEN_BYTES / (time.perf_counter() - t0) / 1e9
+    for nt, reps in ((threads, 3), (1, 1)):
+        rates = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            assert oracle.pack(lay, src_layers, 2 * H * BS * D * E, nb, bt_a, n, pool, ids, nt) == oracle.OK
+            assert oracle.unpack(lay, dst_layers, 2 * H * BS * D * E, nb, bt_b, n, pool, ids, nt) == oracle.OK
+            rates.append(2 * n * TOKEN_BYTES / (time.perf_counter() - t0) / 1e9)
+        res[nt] = statistics.median(rates)
     return {"value": round(res[threads], 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "value_1_thread": round(res[1], 3),
             "sample": f"{n_chunks} chunks ({n:,} tokens, {n * TOKEN_BYTES / 2**30:.0f} GiB per direction) of the "
-                      "128k workload: oracle store then load, host memory to host memory, seeded random bytes"}
+                      "128k workload: oracle store then load, host memory to host memory, seeded random bytes; "
+                      f"median of 3 passes on {threads} threads, 1 pass on 1 thread"}
 
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): this path is measured per "
@@ -229,7 +252,7 @@ def main():
     per_launch = alg_bytes / max(launches, 1)
     roof = None
     if args.mode == "staged":
-        traffic, why = traffic_from_profile()
+        traffic, why = traffic_from_profile(dom)
         achieved = per_launch / (avg_ms / 1e3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,

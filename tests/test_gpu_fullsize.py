@@ -116,7 +116,8 @@ def test_six_turn_session_with_producer_delays():
             tables[prod] = rng.permutation(NB)[:nblk].astype(np.int32)
         else:  # append new blocks to the producer's table from its free blocks
             free = np.setdiff1d(np.arange(NB), tables[prod])
-            tables[prod] = np.concatenate([tables[prod], rng.permutation(free)[:nblk - len(tables[prod])]])
+            extra = rng.permutation(free)[:nblk - len(tables[prod])]
+            tables[prod] = np.concatenate([tables[prod], extra]).astype(np.int32)
         s = streams[prod]
         k0 = lay.nblk(n_prev)
         with torch.cuda.stream(s):

@@ -7,16 +7,17 @@
 // inside plane (l, kv) of the chunk.  The slab is therefore contiguous on both sides and
 // differs only by a permutation of D*E-byte rows: cache row (h, s) <-> chunk row (s, h).
 //
-// Lanes walk the chunk side in order (16 consecutive lanes cover one 256-byte row when
-// D*E = 256), so the pool/staging side -- host memory over PCIe in zero-copy mode -- is
-// touched in fully contiguous 1 KiB-per-wave runs, and the cache side in whole-row
-// 256-byte runs.  Rows are >= 16 bytes and moved as 16-byte vectors, so no LDS transpose
-// is needed for coalescing.  Values are moved as integers only: no float register ever
-// holds them (NaN payloads, -0 and subnormals survive).
+// Lanes walk the write side in order: the chunk side for pack (so the pool/staging side --
+// host memory over PCIe in zero-copy mode -- is written in contiguous 1 KiB-per-wave runs),
+// and the cache side for unpack of whole blocks.  The other side is touched in whole-row
+// runs (256 bytes at D*E = 256).  Rows are >= 16 bytes and moved as 16-byte vectors, so no
+// LDS transpose is needed for coalescing (staging through LDS was measured slower).
+// Values are moved as integers only: no float register ever holds them (NaN payloads, -0
+// and subnormals survive).
 //
-// Each thread keeps U vectors in flight (U loads issued before the U stores).  Index math
-// is wave-uniform except one division at thread start; afterwards every step is an
-// addition with carry.
+// Index math is one division at thread start; afterwards every step is an addition with
+// carry.  Streaming data is read and written nontemporally; device-side launches cap
+// residency at 4 workgroups per CU (see KVX_LDS_RESERVE).
 #include "kvx_internal.h"
 
 namespace kvx {
@@ -26,8 +27,9 @@ namespace {
 // One 16-byte vector as a native 128-bit register tuple (kept in VGPRs; never a float).
 typedef uint32_t vec16 __attribute__((ext_vector_type(4)));
 
-// Compile-time tuning knobs: vectors in flight per thread, and streaming (nontemporal)
-// access on the read and write side.
+// Compile-time tuning knobs: vectors each thread loads before storing (a full tile of
+// kThreads*U vectors; 1 measured best), streaming (nontemporal) access on the read and
+// write side, and the lane order of whole-block unpacks.
 #ifndef KVX_UNROLL
 #define KVX_UNROLL 1
 #endif
@@ -39,6 +41,13 @@ typedef uint32_t vec16 __attribute__((ext_vector_type(4)));
 #endif
 #ifndef KVX_UNPACK_CACHE_ORDER
 #define KVX_UNPACK_CACHE_ORDER 1
+#endif
+// Dynamic LDS reserved per workgroup (never touched) to cap the workgroups resident per CU:
+// 40 KiB of the CU's 160 KiB allows 4 (16 waves per CU).  Measured on MI355X with the
+// 27B-class layout, 4 resident workgroups move slabs faster than 3 or than 6 and more:
+// fewer concurrent 32 KiB streams per CU keep the HBM read/write mix efficient.
+#ifndef KVX_LDS_RESERVE
+#define KVX_LDS_RESERVE 40960
 #endif
 
 __device__ __forceinline__ vec16 load16(const vec16 *p) {
@@ -226,14 +235,6 @@ __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, in
 }
 
 constexpr int kUnroll = KVX_UNROLL;
-
-// Dynamic LDS reserved per workgroup (never touched) to cap the workgroups resident per CU:
-// 40 KiB of the CU's 160 KiB allows 4 (16 waves per CU).  Measured on MI355X with the
-// 27B-class layout, 4 resident workgroups move slabs faster than 3 or than 6 and more:
-// fewer concurrent 32 KiB streams per CU keep the HBM read/write mix efficient.
-#ifndef KVX_LDS_RESERVE
-#define KVX_LDS_RESERVE 40960
-#endif
 
 }  // namespace
 

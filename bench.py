@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--no-256k", action="store_true", help="skip the 256k restore measurement")
     ap.add_argument("--no-zero-copy-compare", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-paper-layout", action="store_true", help="skip the paper-native layout measurement")
+    ap.add_argument("--paper-layout-only", action="store_true",
+                    help="only measure the paper-native layout and print its JSON object (run by the main bench)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (PMC counter scale reference)")
     return ap.parse_args()
@@ -138,6 +141,69 @@ def traffic_from_profile(kernel):
     return float(kv[f"{kernel}_hbm_bytes_per_launch"]), None
 
 
+def paper_layout(np, torch, harness, hg, kvx, mode, dev, reps=3):
+    """The paper's attention KV layout (Table 1, Sec. 3.1): FP8-sized 1-byte elements, 16 layers,
+    4 KV heads, head_dim 256, 32-token pages in token-major (NHD) blocks, 1,568-token chunks;
+    a 131,072-token prefix (32 KiB per token, 4 GiB per direction) stored and restored."""
+    Lp, Hp, Dp, Ep, BSp, Cp = 16, 4, 256, 1, 32, 1568
+    tb = 2 * Lp * Hp * Dp * Ep
+    n, nb = 131072, 5120
+    nc, nblk = -(-n // Cp), -(-n // BSp)
+    layout = kvx.make_layout(Lp, Hp, Dp, Ep, BSp, Cp)
+    seed = harness.sub_seed("bench-paper", n)
+    a = torch.empty((Lp, nb, 2, BSp, Hp, Dp), dtype=torch.uint8, device=dev)
+    b = torch.zeros_like(a)
+    hg.fill_values(a, 0, seed, "raw", 1)
+    bt_a, bt_b = harness.block_table(seed + 1, nb, nblk), harness.block_table(seed + 2, nb, nblk)
+    t_a, t_b = torch.from_numpy(bt_a).to(dev), torch.from_numpy(bt_b).to(dev)
+    ids = harness.chunk_ids(nc, nc)
+    pool = kvx.kv_pool_create(layout, nc, mode, profile=True)
+    ca = kvx.Cache(a, layout, nb, block_order=kvx.KV_BLOCK_NHD)
+    cb = kvx.Cache(b, layout, nb, block_order=kvx.KV_BLOCK_NHD)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    kvx.kv_store(ca, t_a, n, pool, ids, s)
+    kvx.kv_load(cb, t_b, n, pool, ids, s)
+    s.synchronize()
+    for w in ("pack", "unpack"):
+        kvx.kv_pool_kernel_stats(pool, w, reset=True)
+    st, ld, restore = [], [], []
+    for _ in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(s)
+        kvx.kv_store(ca, t_a, n, pool, ids, s)
+        e[1].record(s)
+        kvx.kv_load(cb, t_b, n, pool, ids, s)
+        e[2].record(s)
+        s.synchronize()
+        st.append(e[0].elapsed_time(e[1]) / 1e3)
+        ld.append(e[1].elapsed_time(e[2]) / 1e3)
+    for _ in range(reps):
+        w0 = time.perf_counter()
+        kvx.kv_load(cb, t_b, n, pool, ids, s)
+        s.synchronize()
+        restore.append(time.perf_counter() - w0)
+    N = n * tb
+    kern = {}
+    for w in ("pack", "unpack"):
+        launches, ms, alg = kvx.kv_pool_kernel_stats(pool, w, reset=True)
+        kern[w] = {"launches": launches, "avg_launch_ms": round(ms / max(launches, 1), 4),
+                   "achieved_GBps": round(alg / (ms / 1e3) / 1e9, 1) if ms else None,
+                   "frac_of_hbm_peak": round(alg / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4) if ms else None}
+    ta = torch.from_numpy(bt_a.astype(np.int64)).to(dev)
+    tbb = torch.from_numpy(bt_b.astype(np.int64)).to(dev)
+    ok = all(torch.equal(a[:, ta[k:k + 1024]], b[:, tbb[k:k + 1024]]) for k in range(0, nblk, 1024))
+    kvx.kv_pool_destroy(pool)
+    del a, b
+    torch.cuda.empty_cache()
+    return {"layout": "16 layers, 4 KV heads, head_dim 256, 1-byte elements, 32-token NHD pages, 1,568-token chunks",
+            "prefix_tokens": n, "bytes_per_direction": N, "mode": mode,
+            "store_GBps": round(N / statistics.median(st) / 1e9, 3),
+            "load_GBps": round(N / statistics.median(ld) / 1e9, 3),
+            "restore_s_128k": round(statistics.median(restore), 4), "kernels": kern,
+            "round_trip": "bit-exact (whole prefix, on device)" if ok else "FAILED"}, ok
+
+
 def cpu_baseline(np, oracle, n_chunks=64):
     """The oracle timed on host cores: store + load of a bounded sample of the workload."""
     rng = np.random.default_rng(2609)
@@ -188,6 +254,29 @@ def main():
     from paper_2609_15021_amd import kvx
 
     dev = torch.device("cuda:0")
+    if args.paper_layout_only:
+        paper, paper_ok = paper_layout(np, torch, harness, hg, kvx, args.mode, dev)
+        print(json.dumps(paper), flush=True)
+        sys.exit(0 if paper_ok else 1)
+
+    # The paper-layout leg runs first, in its own process, on fresh memory: on these machines,
+    # transfers through pools created after large allocations were freed measured ~10% slower
+    # (even from a new process), and a serving pool is created once at startup.
+    paper = None
+    if not args.no_paper_layout:
+        import subprocess
+        r = subprocess.run([sys.executable, os.path.abspath(__file__), "--paper-layout-only", "--mode", args.mode],
+                           capture_output=True, text=True, timeout=600)
+        lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
+        paper = json.loads(lines[-1]) if lines else {"error": r.stderr[-2000:]}
+        paper_ok = r.returncode == 0
+        if lines:
+            log(f"[bench] paper layout 128k: store {paper['store_GBps']} GB/s, load {paper['load_GBps']} GB/s, "
+                f"restore {paper['restore_s_128k']} s, pack {paper['kernels']['pack']['achieved_GBps']} GB/s, "
+                f"unpack {paper['kernels']['unpack']['achieved_GBps']} GB/s; {paper['round_trip']}")
+    else:
+        paper_ok = True
+
     layout = kvx.make_layout(L, H, D, E, BS, C)
     n = args.tokens
     nc = -(-n // C)
@@ -208,7 +297,8 @@ def main():
     info = kvx.kv_pool_get_info(pool)
     torch.cuda.synchronize()
     log(f"[bench] pool {info['pool_bytes'] / 2**30:.1f} GiB pinned={info['is_pinned']} "
-        f"alloc {info['alloc_seconds']:.3f} s; staging {info['staging_bytes'] / 2**30:.1f} GiB")
+        f"alloc {info['alloc_seconds']:.3f} s; staging {info['staging_bytes'] / 2**30:.1f} GiB "
+        f"(contiguous={info['staging_contiguous']})")
 
     peak = link_peak(torch, hg, info["host_base"], 1 << 30, dev)
     log(f"[bench] pinned hipMemcpyAsync peak: D2H {peak['d2h']:.2f} GB/s, H2D {peak['h2d']:.2f} GB/s")
@@ -271,6 +361,7 @@ def main():
 
     ok, parity_msg = sampled_round_trip(np, harness, rep_b, bt_a, bt_b, seed, n, args.pool_blocks,
                                         sorted({0, nc // 2, nc - 1}), torch)
+    ok = ok and paper_ok
     log(f"[bench] parity: {parity_msg}")
 
     # Restore seconds: host wall clock of a full-prefix load (prefix already in the pool).
@@ -297,6 +388,7 @@ def main():
             kvx.kv_pool_set_mode(pool, args.mode)
             log(f"[bench] {other_mode}: store {zc['store_GBps']} GB/s, load {zc['load_GBps']} GB/s")
     alloc_s = info["alloc_seconds"]
+    staging_contig = info["staging_contiguous"]
     kvx.kv_pool_destroy(pool)
     del rep_a, rep_b, t_a, t_b
     torch.cuda.empty_cache()
@@ -361,8 +453,10 @@ def main():
         "roofline": roof,
         "zero_copy_compare": zc,
         "pool_alloc_s": round(alloc_s, 4),
+        "staging_contiguous": bool(staging_contig),
         "parity": parity_msg if ok else f"FAILED: {parity_msg}",
         "parity_256k": parity_256k,
+        "paper_layout": paper,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

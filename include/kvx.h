@@ -22,8 +22,11 @@
  *  Cache: layer l is one device buffer layer_ptrs[l] holding num_blocks blocks,
  *    block b at byte b*block_stride.  Inside a block, element (kv, h, s, d) is at
  *    ((kv*H + h)*BS + s)*D*E + d*E, i.e. [2][H][BS][D] ("HND", kv 0 = K, 1 = V;
- *    the paper's replicas run HND, Table 1).  Token t of a prefix lives in block
- *    block_table[t / BS] at slot t % BS.
+ *    the paper's replicas run HND, Table 1), or with block_order KV_BLOCK_NHD at
+ *    ((kv*BS + s)*H + h)*D*E + d*E, i.e. [2][BS][H][D] (the token-major variant
+ *    the paper's patch could not read, Sec. 3.1).  Token t of a prefix lives in
+ *    block block_table[t / BS] at slot t % BS.  The chunk format below does not
+ *    depend on the block order: caches of either order share one pool.
  *
  *  Chunks: a prefix of n tokens is cut into nc = ceil(n / C) chunks; chunk i
  *    holds tokens [i*C, i*C + r_i), r_i = min(C, n - i*C) (only the last chunk
@@ -80,6 +83,10 @@ typedef int32_t kv_status;
 #define KV_HOST_COHERENT 0u     /* fine-grained pinned memory (default) */
 #define KV_HOST_NONCOHERENT 1u  /* coarse-grained pinned memory */
 
+/* Token order inside a cache block (kv_cache.block_order). */
+#define KV_BLOCK_HND 0  /* [2][H][BS][D] */
+#define KV_BLOCK_NHD 1  /* [2][BS][H][D] */
+
 /* Async error bits reported by kv_pool_async_error. */
 #define KV_ASYNC_BAD_BLOCK 1   /* a block_table entry was outside [0, num_blocks): no cache byte of it was
                                   touched; a store wrote zeros for its chunk rows */
@@ -99,6 +106,8 @@ typedef struct kv_cache {
     kv_layout layout;
     int32_t num_blocks;          /* blocks per layer buffer */
     int32_t device;              /* HIP device ordinal the buffers live on */
+    int32_t block_order;         /* KV_BLOCK_HND or KV_BLOCK_NHD */
+    int32_t reserved;            /* must be 0 */
     void *const *layer_ptrs;     /* HOST array of num_layers DEVICE pointers, read during the call only */
     int64_t block_stride_bytes;  /* bytes between blocks; 0 = packed (2*H*BS*D*E) */
 } kv_cache;
@@ -130,7 +139,7 @@ typedef struct kv_pool_info {
     int32_t staging_slots;
     int32_t chunks_per_batch;
     int32_t side_streams;
-    int32_t reserved;
+    int32_t staging_contiguous; /* 1: staging is one physically contiguous device allocation */
     void *host_base;           /* host address of slot 0 */
     void *device_base;         /* device address of slot 0 (mapped pinned memory) */
 } kv_pool_info;
@@ -186,7 +195,8 @@ KV_API kv_status kv_pool_kernel_stats(kv_pool *pool, int which, int reset, int64
  * Host-only validation of a store/load request, no HIP call (Sec. 3.1: layout
  * constraints are validated, never inferred).  Checks: cache layout equals
  * pool_layout field by field; positive sizes; E in {1,2,4}; C % BS == 0;
- * block_stride 0 or >= 2*H*BS*D*E; n_tokens >= 0; for n_tokens > 0 non-NULL
+ * block_stride 0 or >= 2*H*BS*D*E; block_order KV_BLOCK_HND or KV_BLOCK_NHD
+ * and reserved 0; n_tokens >= 0; for n_tokens > 0 non-NULL
  * layer pointers and chunk_ids, chunk ids in [0, pool_slots), and for a store
  * pairwise distinct (duplicates make the result order dependent).  GPU-path
  * limits give KV_EUNSUPPORTED: D*E % 16 != 0, a layer pointer or

@@ -32,6 +32,8 @@ _LIB_OVERRIDE = os.environ.get("KVX_ORACLE_LIB")
 
 OK = 0
 EINVAL = -1
+BLOCK_HND = 0  # cache block [2][H][BS][D]
+BLOCK_NHD = 1  # cache block [2][BS][H][D]
 
 
 def build(verbose: bool = False) -> str:
@@ -69,7 +71,7 @@ def _load():
     lib.oracle_validate.argtypes = [ctypes.POINTER(OracleLayout), i64, i64, P, i64, i64, P, ctypes.c_int]
     lib.oracle_validate.restype = ctypes.c_int
     for fn in (lib.oracle_pack, lib.oracle_unpack):
-        fn.argtypes = [ctypes.POINTER(OracleLayout), P, i64, i64, P, i64, P, i64, P, ctypes.c_int]
+        fn.argtypes = [ctypes.POINTER(OracleLayout), ctypes.c_int, P, i64, i64, P, i64, P, i64, P, ctypes.c_int]
         fn.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -108,7 +110,8 @@ def validate(lay, num_blocks, block_stride, block_table, n_tokens, num_slots, ch
                                        int(n_tokens), int(num_slots), _ptr(ci), int(bool(for_pack))))
 
 
-def pack(lay, layers, block_stride, num_blocks, block_table, n_tokens, pool, chunk_ids, nthreads=1):
+def pack(lay, layers, block_stride, num_blocks, block_table, n_tokens, pool, chunk_ids, nthreads=1,
+         block_order=BLOCK_HND):
     """Store: cache layers (list of L host byte arrays) -> pool (uint8, num_slots*slot_bytes)."""
     for k, a in enumerate(layers):
         _check_bytes(a, f"layers[{k}]")
@@ -117,12 +120,13 @@ def pack(lay, layers, block_stride, num_blocks, block_table, n_tokens, pool, chu
     num_slots = pool.nbytes // sb
     bt = np.ascontiguousarray(block_table, dtype=np.int32)
     ci = np.ascontiguousarray(chunk_ids, dtype=np.int64)
-    return int(_load().oracle_pack(ctypes.byref(lay), _layer_ptr_array(layers), int(num_blocks),
+    return int(_load().oracle_pack(ctypes.byref(lay), int(block_order), _layer_ptr_array(layers), int(num_blocks),
                                    int(block_stride), _ptr(bt), int(n_tokens), _ptr(pool),
                                    int(num_slots), _ptr(ci), int(nthreads)))
 
 
-def unpack(lay, layers, block_stride, num_blocks, block_table, n_tokens, pool, chunk_ids, nthreads=1):
+def unpack(lay, layers, block_stride, num_blocks, block_table, n_tokens, pool, chunk_ids, nthreads=1,
+           block_order=BLOCK_HND):
     """Load: pool -> cache layers (list of L writable host byte arrays)."""
     for k, a in enumerate(layers):
         _check_bytes(a, f"layers[{k}]", writable=True)
@@ -131,6 +135,6 @@ def unpack(lay, layers, block_stride, num_blocks, block_table, n_tokens, pool, c
     num_slots = pool.nbytes // sb
     bt = np.ascontiguousarray(block_table, dtype=np.int32)
     ci = np.ascontiguousarray(chunk_ids, dtype=np.int64)
-    return int(_load().oracle_unpack(ctypes.byref(lay), _layer_ptr_array(layers), int(num_blocks),
+    return int(_load().oracle_unpack(ctypes.byref(lay), int(block_order), _layer_ptr_array(layers), int(num_blocks),
                                      int(block_stride), _ptr(bt), int(n_tokens), _ptr(pool),
                                      int(num_slots), _ptr(ci), int(nthreads)))

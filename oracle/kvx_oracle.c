@@ -72,6 +72,7 @@ int oracle_validate(const oracle_layout *lay, int64_t num_blocks, int64_t block_
 /* Everything one worker needs; chunks [first, last) are its share. */
 typedef struct oracle_job {
     const oracle_layout *lay;
+    int block_order;
     uint8_t *const *cache_layers; /* written by unpack, read by pack */
     int64_t block_stride;
     const int32_t *block_table;
@@ -83,11 +84,13 @@ typedef struct oracle_job {
 } oracle_job;
 
 /* Byte offset of cache row (kv, h, slot s) inside block b of one layer. */
-static int64_t cache_row_offset(const oracle_layout *lay, int64_t block_stride, int64_t b,
-                                int64_t kv, int64_t h, int64_t s)
+static int64_t cache_row_offset(const oracle_layout *lay, int block_order, int64_t block_stride,
+                                int64_t b, int64_t kv, int64_t h, int64_t s)
 {
     int64_t H = lay->num_kv_heads, BS = lay->block_size;
     int64_t row_bytes = (int64_t)lay->head_dim * lay->elem_bytes;
+    if (block_order == ORACLE_BLOCK_NHD)
+        return b * block_stride + ((kv * BS + s) * H + h) * row_bytes;
     return b * block_stride + ((kv * H + h) * BS + s) * row_bytes;
 }
 
@@ -121,7 +124,8 @@ static void *oracle_worker(void *arg)
                     int64_t b = job->block_table[t / BS];
                     int64_t s = t % BS;
                     for (int64_t h = 0; h < H; ++h) {
-                        uint8_t *cache_row = layer + cache_row_offset(lay, job->block_stride, b, kv, h, s);
+                        uint8_t *cache_row =
+                            layer + cache_row_offset(lay, job->block_order, job->block_stride, b, kv, h, s);
                         uint8_t *chunk_row = slot + chunk_row_offset(lay, r, l, kv, u, h);
                         if (job->to_pool)
                             memcpy(chunk_row, cache_row, (size_t)row_bytes);
@@ -135,11 +139,13 @@ static void *oracle_worker(void *arg)
     return NULL;
 }
 
-static int oracle_run(const oracle_layout *lay, uint8_t *const *layers, int64_t num_blocks,
-                      int64_t block_stride, const int32_t *block_table, int64_t n_tokens,
-                      uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids, int nthreads,
-                      int to_pool)
+static int oracle_run(const oracle_layout *lay, int block_order, uint8_t *const *layers,
+                      int64_t num_blocks, int64_t block_stride, const int32_t *block_table,
+                      int64_t n_tokens, uint8_t *pool, int64_t num_slots,
+                      const int64_t *chunk_ids, int nthreads, int to_pool)
 {
+    if (block_order != ORACLE_BLOCK_HND && block_order != ORACLE_BLOCK_NHD)
+        return ORACLE_EINVAL;
     int rc = oracle_validate(lay, num_blocks, block_stride, block_table, n_tokens, num_slots,
                              chunk_ids, to_pool);
     if (rc != ORACLE_OK)
@@ -167,6 +173,7 @@ static int oracle_run(const oracle_layout *lay, uint8_t *const *layers, int64_t 
     }
     for (int k = 0; k < nthreads; ++k) {
         jobs[k].lay = lay;
+        jobs[k].block_order = block_order;
         jobs[k].cache_layers = layers;
         jobs[k].block_stride = block_stride;
         jobs[k].block_table = block_table;
@@ -194,20 +201,22 @@ static int oracle_run(const oracle_layout *lay, uint8_t *const *layers, int64_t 
     return ORACLE_OK;
 }
 
-int oracle_pack(const oracle_layout *lay, const uint8_t *const *layer_ptrs, int64_t num_blocks,
-                int64_t block_stride, const int32_t *block_table, int64_t n_tokens,
-                uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids, int nthreads)
+int oracle_pack(const oracle_layout *lay, int block_order, const uint8_t *const *layer_ptrs,
+                int64_t num_blocks, int64_t block_stride, const int32_t *block_table,
+                int64_t n_tokens, uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids,
+                int nthreads)
 {
     /* The cache is only read in this direction. */
-    return oracle_run(lay, (uint8_t *const *)layer_ptrs, num_blocks, block_stride, block_table,
-                      n_tokens, pool, num_slots, chunk_ids, nthreads, 1);
+    return oracle_run(lay, block_order, (uint8_t *const *)layer_ptrs, num_blocks, block_stride,
+                      block_table, n_tokens, pool, num_slots, chunk_ids, nthreads, 1);
 }
 
-int oracle_unpack(const oracle_layout *lay, uint8_t *const *layer_ptrs, int64_t num_blocks,
-                  int64_t block_stride, const int32_t *block_table, int64_t n_tokens,
-                  const uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids, int nthreads)
+int oracle_unpack(const oracle_layout *lay, int block_order, uint8_t *const *layer_ptrs,
+                  int64_t num_blocks, int64_t block_stride, const int32_t *block_table,
+                  int64_t n_tokens, const uint8_t *pool, int64_t num_slots,
+                  const int64_t *chunk_ids, int nthreads)
 {
     /* The pool is only read in this direction. */
-    return oracle_run(lay, layer_ptrs, num_blocks, block_stride, block_table, n_tokens,
-                      (uint8_t *)pool, num_slots, chunk_ids, nthreads, 0);
+    return oracle_run(lay, block_order, layer_ptrs, num_blocks, block_stride, block_table,
+                      n_tokens, (uint8_t *)pool, num_slots, chunk_ids, nthreads, 0);
 }

@@ -13,8 +13,10 @@
  *   1,568-token logical block is 49 pages of 32 tokens).
  *
  * Cache element (l, b, kv, h, s, d) sits at byte
- *     b*block_stride + ((kv*H + h)*BS + s)*D*E + d*E      of layer_ptrs[l]
- * (per-layer [NB][2][H][BS][D], "HND" as in the paper's Table 1; kv 0 = K).
+ *     b*block_stride + ((kv*H + h)*BS + s)*D*E + d*E      of layer_ptrs[l]   (block_order 0)
+ * (per-layer [NB][2][H][BS][D], "HND" as in the paper's Table 1; kv 0 = K), or at
+ *     b*block_stride + ((kv*BS + s)*H + h)*D*E + d*E                       (block_order 1)
+ * (per-layer [NB][2][BS][H][D], "NHD", the layout the paper's patch rejected, Sec. 3.1).
  * Token t lives in block bt[t / BS], slot t % BS.
  * Chunk i (of nc = ceil(n / C)) holds tokens [i*C, i*C + r_i), r_i = min(C, n - i*C),
  * packed plane-major [L][2][r_i][H][D] at pool + chunk_ids[i]*slot_bytes,
@@ -40,6 +42,10 @@ typedef struct oracle_layout {
     int32_t chunk_tokens; /* C : tokens per packed chunk */
 } oracle_layout;
 
+/* Token order inside a cache block. */
+#define ORACLE_BLOCK_HND 0 /* [2][H][BS][D] */
+#define ORACLE_BLOCK_NHD 1 /* [2][BS][H][D] */
+
 /* Error codes (negative). */
 #define ORACLE_OK 0
 #define ORACLE_EINVAL (-1)
@@ -60,18 +66,21 @@ int oracle_validate(const oracle_layout *lay, int64_t num_blocks, int64_t block_
 
 /*
  * Pack (store): copy every named token row of the cache into its chunk row.
+ * block_order: ORACLE_BLOCK_HND or ORACLE_BLOCK_NHD (anything else is ORACLE_EINVAL).
  * layer_ptrs: L host pointers.  pool: num_slots * slot_bytes host bytes.
  * nthreads >= 1: chunks are split over that many POSIX threads (each chunk is
  * independent).  Returns ORACLE_OK or ORACLE_EINVAL (nothing written then).
  */
-int oracle_pack(const oracle_layout *lay, const uint8_t *const *layer_ptrs, int64_t num_blocks,
-                int64_t block_stride, const int32_t *block_table, int64_t n_tokens,
-                uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids, int nthreads);
+int oracle_pack(const oracle_layout *lay, int block_order, const uint8_t *const *layer_ptrs,
+                int64_t num_blocks, int64_t block_stride, const int32_t *block_table,
+                int64_t n_tokens, uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids,
+                int nthreads);
 
 /* Unpack (load): the exact inverse of oracle_pack. */
-int oracle_unpack(const oracle_layout *lay, uint8_t *const *layer_ptrs, int64_t num_blocks,
-                  int64_t block_stride, const int32_t *block_table, int64_t n_tokens,
-                  const uint8_t *pool, int64_t num_slots, const int64_t *chunk_ids, int nthreads);
+int oracle_unpack(const oracle_layout *lay, int block_order, uint8_t *const *layer_ptrs,
+                  int64_t num_blocks, int64_t block_stride, const int32_t *block_table,
+                  int64_t n_tokens, const uint8_t *pool, int64_t num_slots,
+                  const int64_t *chunk_ids, int nthreads);
 
 #ifdef __cplusplus
 }

@@ -91,6 +91,10 @@ kv_status check_request(const kv_cache *cache, const kv_layout *pool_layout, int
                     pool_layout->elem_bytes, pool_layout->block_size, pool_layout->chunk_tokens);
     if (cache->num_blocks <= 0)
         return fail(KV_EINVAL, "num_blocks must be positive (got %d)", cache->num_blocks);
+    if (cache->block_order != KV_BLOCK_HND && cache->block_order != KV_BLOCK_NHD)
+        return fail(KV_EINVAL, "block_order must be KV_BLOCK_HND or KV_BLOCK_NHD (got %d)", cache->block_order);
+    if (cache->reserved != 0)
+        return fail(KV_EINVAL, "kv_cache.reserved must be 0");
     const Geometry g = geometry(cache->layout, cache->block_stride_bytes);
     if (cache->block_stride_bytes != 0 && cache->block_stride_bytes < g.block_bytes)
         return fail(KV_EINVAL, "block_stride_bytes %lld is smaller than one block (%lld bytes)",

@@ -7,7 +7,9 @@
 // inside plane (l, kv) of the chunk.  The slab is therefore contiguous on both sides and
 // differs only by a permutation of D*E-byte rows: cache row (h, s) <-> chunk row (s, h).
 //
-// Lanes walk the write side in order: the chunk side for pack (so the pool/staging side --
+// Token-major (NHD) cache blocks hold the slab's rows already in chunk order: the slab
+// is then a straight contiguous copy.  For HND blocks, lanes walk the write side in
+// order: the chunk side for pack (so the pool/staging side --
 // host memory over PCIe in zero-copy mode -- is written in contiguous 1 KiB-per-wave runs),
 // and the cache side for unpack of whole blocks.  The other side is touched in whole-row
 // runs (256 bytes at D*E = 256).  Rows are >= 16 bytes and moved as 16-byte vectors, so no
@@ -169,6 +171,16 @@ __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, in
     vec16 *cache_v = reinterpret_cast<vec16 *>(cache_slab);
 
     const int tid = static_cast<int>(threadIdx.x);
+    if (a.nhd) {
+        // Token-major block: the slab's first bs*H rows are already in chunk row order.
+        for (int v = tid; v < nvec; v += kThreads) {
+            if (DIR == kPack)
+                store16(chunk_v + v, load16(cache_v + v));
+            else
+                store16(cache_v + v, load16(chunk_v + v));
+        }
+        return;
+    }
     if (DIR == kUnpack && KVX_UNPACK_CACHE_ORDER && bs == a.BS) {
         // Whole block: lanes walk the cache side in order, so the writes are the contiguous side.
         RowWalker w(tid, a.vec_per_row, a.BS);

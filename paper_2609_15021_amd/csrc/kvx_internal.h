@@ -51,6 +51,7 @@ struct GatherArgs {
     int32_t vec_per_row;
     int32_t blocks_per_chunk;
     int32_t nchunks;
+    int32_t nhd;                       // cache blocks are [2][BS][H][D] (token-major)
     int32_t slot[kMaxLaunchChunks];    // slot id of each chunk of the launch
 };
 
@@ -99,6 +100,7 @@ struct kv_pool {
     // Staging ring (staged mode).
     int K = 0, cpb = 0, S = 0;
     uint8_t *staging = nullptr;     // K slots of cpb*slot_bytes each
+    bool staging_contiguous = false;  // physically contiguous allocation granted
     std::vector<hipStream_t> sides;
     std::vector<hipEvent_t> ev_free;   // staging slot k may be overwritten once this completes
     std::vector<bool> free_recorded;

@@ -31,6 +31,8 @@ KV_MODE_STAGED = 2
 KV_HOST_COHERENT = 0
 KV_HOST_NONCOHERENT = 1
 KV_ASYNC_BAD_BLOCK = 1
+KV_BLOCK_HND = 0
+KV_BLOCK_NHD = 1
 
 MODES = {"zero_copy": KV_MODE_ZERO_COPY, "staged": KV_MODE_STAGED}
 
@@ -43,6 +45,7 @@ class KvLayout(ctypes.Structure):
 
 class KvCache(ctypes.Structure):
     _fields_ = [("layout", KvLayout), ("num_blocks", ctypes.c_int32), ("device", ctypes.c_int32),
+                ("block_order", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("layer_ptrs", ctypes.POINTER(ctypes.c_void_p)), ("block_stride_bytes", ctypes.c_int64)]
 
 
@@ -59,7 +62,7 @@ class KvPoolInfo(ctypes.Structure):
                 ("mode", ctypes.c_uint32), ("host_kind", ctypes.c_uint32),
                 ("is_pinned", ctypes.c_int32), ("staging_slots", ctypes.c_int32),
                 ("chunks_per_batch", ctypes.c_int32), ("side_streams", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("host_base", ctypes.c_void_p),
+                ("staging_contiguous", ctypes.c_int32), ("host_base", ctypes.c_void_p),
                 ("device_base", ctypes.c_void_p)]
 
 
@@ -120,7 +123,7 @@ def kv_version() -> str:
 
 def _raise(status: int):
     if status != KV_OK:
-        raise KvError(status, f"{kv_status_name(status)}: {kv_last_error()}")
+        raise KvError(status, kv_last_error() or kv_status_name(status))
 
 
 def make_layout(L, H, D, E, BS, C) -> KvLayout:
@@ -130,11 +133,13 @@ def make_layout(L, H, D, E, BS, C) -> KvLayout:
 class Cache:
     """A replica's paged cache as the C ABI sees it (keeps the tensors and pointer array alive).
 
-    ``layers``: one tensor [L][NB][2][H][BS][D] (any dtype of elem_bytes), or a list of L
-    per-layer tensors [NB][...]; ``block_stride_bytes`` 0 means packed blocks.
+    ``layers``: one tensor [L][NB][2][H][BS][D] ([L][NB][2][BS][H][D] with block_order
+    KV_BLOCK_NHD; any dtype of elem_bytes), or a list of L per-layer tensors [NB][...];
+    ``block_stride_bytes`` 0 means packed blocks.
     """
 
-    def __init__(self, layers, layout: KvLayout, num_blocks: int, block_stride_bytes: int = 0):
+    def __init__(self, layers, layout: KvLayout, num_blocks: int, block_stride_bytes: int = 0,
+                 block_order: int = KV_BLOCK_HND):
         if isinstance(layers, torch.Tensor):
             tensors = [layers[l] for l in range(layers.shape[0])]
             self._keep = [layers]
@@ -153,7 +158,8 @@ class Cache:
                 raise ValueError(f"layer {k}: need a contiguous device buffer of >= {need} bytes on {dev}")
         self._ptrs = (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
         self.struct = KvCache(layout, int(num_blocks), int(dev.index if dev.index is not None else 0),
-                              ctypes.cast(self._ptrs, ctypes.POINTER(ctypes.c_void_p)), int(block_stride_bytes))
+                              int(block_order), 0, ctypes.cast(self._ptrs, ctypes.POINTER(ctypes.c_void_p)),
+                              int(block_stride_bytes))
         self.layout = layout
 
 

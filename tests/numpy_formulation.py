@@ -30,3 +30,13 @@ def scatter_tokens(B: np.ndarray, bt: np.ndarray, tv: np.ndarray, BS: int) -> No
     blocks = np.asarray(bt, dtype=np.int64)[t // BS]
     slots = t % BS
     B[:, blocks, :, :, slots, :] = tv.transpose(2, 0, 1, 3, 4)
+
+
+def token_view_nhd(A: np.ndarray, bt: np.ndarray, n: int, BS: int) -> np.ndarray:
+    """[L][2][n][H][D] for a token-major ("NHD") cache A[L][NB][2][BS][H][D]."""
+    t = np.arange(n)
+    blocks = np.asarray(bt, dtype=np.int64)[t // BS]
+    slots = t % BS
+    # Index dims 1 and 3 with arrays (separated by a slice): result [n][L][2][H][D].
+    g = A[:, blocks, :, slots, :, :]
+    return np.ascontiguousarray(g.transpose(1, 2, 0, 3, 4))

@@ -47,10 +47,11 @@ def test_header_compiles_as_plain_c(tmp_path):
                     "-o", str(tmp_path / "t.o")], check=True)
 
 
-def _fake_cache(kvx, layout, num_blocks=64, stride=0, ptr_base=0x7F0000000000, align=16):
+def _fake_cache(kvx, layout, num_blocks=64, stride=0, ptr_base=0x7F0000000000, align=16, order=0, reserved=0):
     ptrs = (ctypes.c_void_p * layout.num_layers)(*[ptr_base + l * (1 << 30) + (align % 16) for l in
                                                     range(layout.num_layers)])
-    c = kvx.KvCache(layout, num_blocks, 0, ctypes.cast(ptrs, ctypes.POINTER(ctypes.c_void_p)), stride)
+    c = kvx.KvCache(layout, num_blocks, 0, order, reserved, ctypes.cast(ptrs, ctypes.POINTER(ctypes.c_void_p)),
+                    stride)
     c._keep = ptrs
     return c
 
@@ -88,6 +89,9 @@ def test_kv_check_rules():
     assert _check(kvx, _fake_cache(kvx, lay, stride=8192 + 16), lay, 4, 10, [0], True) == kvx.KV_OK
     assert _check(kvx, _fake_cache(kvx, lay, align=8), lay, 4, 10, [0], True) == kvx.KV_EUNSUPPORTED
     assert _check(kvx, _fake_cache(kvx, lay, num_blocks=0), lay, 4, 10, [0], True) == kvx.KV_EINVAL
+    assert _check(kvx, _fake_cache(kvx, lay, order=kvx.KV_BLOCK_NHD), lay, 4, 10, [0], True) == kvx.KV_OK
+    assert _check(kvx, _fake_cache(kvx, lay, order=2), lay, 4, 10, [0], True) == kvx.KV_EINVAL
+    assert _check(kvx, _fake_cache(kvx, lay, reserved=1), lay, 4, 10, [0], True) == kvx.KV_EINVAL
 
 
 def test_kv_check_agrees_with_oracle_validation():

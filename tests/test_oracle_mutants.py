@@ -25,7 +25,10 @@ MUTANTS = {
     "unpack_copies_wrong_way": ("memcpy(cache_row, chunk_row, (size_t)row_bytes);",
                                 "memcpy(chunk_row, cache_row, (size_t)row_bytes);"),
     "divisibility_check_dropped": ("if (lay->chunk_tokens % lay->block_size != 0)", "if (0)"),
-    "head_and_slot_swapped": ("((kv * H + h) * BS + s) * row_bytes", "((kv * BS + s) * H + h) * row_bytes"),
+    "head_and_slot_swapped": ("return b * block_stride + ((kv * H + h) * BS + s) * row_bytes;",
+                              "return b * block_stride + ((kv * BS + s) * H + h) * row_bytes;"),
+    "nhd_read_as_hnd": ("return b * block_stride + ((kv * BS + s) * H + h) * row_bytes;",
+                        "return b * block_stride + ((kv * H + h) * BS + s) * row_bytes;"),
 }
 
 
@@ -33,7 +36,7 @@ MUTANTS = {
 def test_pins_catch_mutant(name, tmp_path):
     old, new = MUTANTS[name]
     src = open(SRC).read()
-    assert src.count(old) >= 1, f"mutation anchor for {name} not found in the oracle source"
+    assert src.count(old) == 1, f"mutation anchor for {name} must occur exactly once in the oracle source"
     mutated = tmp_path / "mut.c"
     mutated.write_text(src.replace(old, new))
     lib = tmp_path / "libmut.so"
@@ -41,6 +44,7 @@ def test_pins_catch_mutant(name, tmp_path):
                     "-o", str(lib), str(mutated), "-lpthread"], check=True)
     env = dict(os.environ, KVX_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_nhd.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"

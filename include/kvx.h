@@ -159,7 +159,8 @@ typedef struct kv_pool_info {
 KV_API kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_pool_options *opts,
                          kv_pool **out);
 
-/* Waits for the pool's own side streams, then frees everything.  NULL is a no-op. */
+/* Waits until every store/load enqueued on the pool has completed on its caller stream
+ * and the pool's side streams are idle, then frees everything.  NULL is a no-op. */
 KV_API kv_status kv_pool_destroy(kv_pool *pool);
 
 /* Fills *info.  KV_EINVAL on NULL arguments. */

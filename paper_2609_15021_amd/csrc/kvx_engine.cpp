@@ -35,6 +35,11 @@ kv_status release(kv_pool *p) {
         if (e != hipSuccess && first == KV_OK)
             first = kvx::hip_fail(e, what, __FILE__, __LINE__);
     };
+    // Work queued on caller streams (kernels writing the pool or staging) must finish first.
+    for (auto &use : p->last_use)
+        note(hipEventSynchronize(use.second), "hipEventSynchronize(last use)");
+    for (auto &use : p->last_use)
+        note(hipEventDestroy(use.second), "hipEventDestroy");
     for (hipStream_t s : p->sides)
         note(hipStreamSynchronize(s), "hipStreamSynchronize(side)");
     for (hipStream_t s : p->sides)
@@ -264,6 +269,22 @@ kv_status transfer(kv_pool *p, const kv_cache *cache, const int32_t *block_table
     return KV_OK;
 }
 
+// Record the pool's last use on `stream` (one event per stream seen).
+kv_status mark_use(kv_pool *p, hipStream_t stream) {
+    for (auto &use : p->last_use)
+        if (use.first == stream) {
+            KVX_HIP(hipEventRecord(use.second, stream));
+            return KV_OK;
+        }
+    hipEvent_t e = nullptr;
+    kv_status st = make_event(&e, false);
+    if (st != KV_OK)
+        return st;
+    p->last_use.emplace_back(stream, e);
+    KVX_HIP(hipEventRecord(e, stream));
+    return KV_OK;
+}
+
 kv_status run(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, kv_pool *pool,
               const int64_t *chunk_ids, void *stream, Direction dir) {
     if (!pool)
@@ -280,7 +301,11 @@ kv_status run(const kv_cache *cache, const int32_t *block_table, int64_t n_token
     st = check_device(pool, cache);
     if (st != KV_OK)
         return st;
-    return transfer(pool, cache, block_table, n_tokens, chunk_ids, static_cast<hipStream_t>(stream), dir);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = transfer(pool, cache, block_table, n_tokens, chunk_ids, s, dir);
+    // Record the last use on this stream even after a partial enqueue.
+    const kv_status st_use = mark_use(pool, s);
+    return st != KV_OK ? st : st_use;
 }
 
 }  // namespace

@@ -109,6 +109,9 @@ struct kv_pool {
     hipEvent_t ev_entry = nullptr;     // entry gate of a load
     int ring = 0;
     int zc_chunks = 0;                 // chunks per zero-copy launch
+    // Last use of the pool on each caller stream (recorded after every store/load), so that
+    // kv_pool_destroy never frees memory that queued kernels or copies still touch.
+    std::vector<std::pair<hipStream_t, hipEvent_t>> last_use;
 
     // Profiling of pack/unpack launches.
     bool profile = false;

@@ -7,8 +7,10 @@ plain C library ``libkvx_oracle.so`` built from ``kvx_oracle.c`` with gcc.
 
 What the oracle computes is the plain definition of the paper's state transfer
 (Sec. 2.2: KV state as opaque bytes; Sec. 3.1: a logical chunk spans a whole
-number of paged blocks, and the layout is validated rather than inferred).  See
-``kvx_oracle.h`` for the exact byte-level definition.
+number of paged blocks, and the layout is validated rather than inferred), and
+the hybrid model's recurrent-state snapshot pages moved as opaque bytes (Sec.
+2.2).  See ``kvx_oracle.h`` for the exact byte-level definitions, and
+``recovery.py`` for the aligned-recovery rule.
 
 Every function here is pinned by ``tests/test_oracle_*.py`` against values and
 properties the paper and the mathematics fix (numpy fancy-indexing
@@ -72,6 +74,11 @@ def _load():
     lib.oracle_validate.restype = ctypes.c_int
     for fn in (lib.oracle_pack, lib.oracle_unpack):
         fn.argtypes = [ctypes.POINTER(OracleLayout), ctypes.c_int, P, i64, i64, P, i64, P, i64, P, ctypes.c_int]
+        fn.restype = ctypes.c_int
+    lib.oracle_state_validate.argtypes = [i64, i64, i64, i64, P, i64, i64, P, ctypes.c_int]
+    lib.oracle_state_validate.restype = ctypes.c_int
+    for fn in (lib.oracle_state_pack, lib.oracle_state_unpack):
+        fn.argtypes = [i64, i64, i64, i64, P, P, i64, P, i64, P]
         fn.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -138,3 +145,41 @@ def unpack(lay, layers, block_stride, num_blocks, block_table, n_tokens, pool, c
     return int(_load().oracle_unpack(ctypes.byref(lay), int(block_order), _layer_ptr_array(layers), int(num_blocks),
                                      int(block_stride), _ptr(bt), int(n_tokens), _ptr(pool),
                                      int(num_slots), _ptr(ci), int(nthreads)))
+
+
+# ---- Recurrent-state snapshot pages (Sec. 2.2); definition in kvx_oracle.h ----
+
+def state_validate(num_layers, page_bytes, page_stride, num_pages, pages, n, num_state_slots, slot_ids, for_pack):
+    pg = None if pages is None else np.ascontiguousarray(pages, dtype=np.int64)
+    si = None if slot_ids is None else np.ascontiguousarray(slot_ids, dtype=np.int64)
+    return int(_load().oracle_state_validate(int(num_layers), int(page_bytes), int(page_stride), int(num_pages),
+                                             _ptr(pg), int(n), int(num_state_slots), _ptr(si),
+                                             int(bool(for_pack))))
+
+
+def _state_call(fn, layers, page_bytes, page_stride, pages, state_pool, slot_ids, writable_layers):
+    for k, a in enumerate(layers):
+        _check_bytes(a, f"layers[{k}]", writable=writable_layers)
+    _check_bytes(state_pool, "state_pool", writable=not writable_layers)
+    G = len(layers)
+    num_pages = min(a.nbytes for a in layers) // page_stride if G else 0
+    # A last page needs only page_bytes, not a whole stride.
+    if G and min(a.nbytes for a in layers) - num_pages * page_stride >= page_bytes:
+        num_pages += 1
+    num_state_slots = state_pool.nbytes // (G * page_bytes) if G and page_bytes > 0 else 0
+    pg = np.ascontiguousarray(pages, dtype=np.int64)
+    si = np.ascontiguousarray(slot_ids, dtype=np.int64)
+    return int(fn(int(G), int(page_bytes), int(page_stride), int(num_pages), _layer_ptr_array(layers), _ptr(pg),
+                  int(pg.size), _ptr(state_pool), int(num_state_slots), _ptr(si)))
+
+
+def state_pack(layers, page_bytes, page_stride, pages, state_pool, slot_ids):
+    """Store snapshots: pages[k] of every layer (list of G host byte arrays) -> state slot slot_ids[k]."""
+    return _state_call(_load().oracle_state_pack, layers, page_bytes, page_stride, pages, state_pool, slot_ids,
+                       False)
+
+
+def state_unpack(layers, page_bytes, page_stride, pages, state_pool, slot_ids):
+    """Load snapshots: state slot slot_ids[k] -> pages[k] of every layer."""
+    return _state_call(_load().oracle_state_unpack, layers, page_bytes, page_stride, pages, state_pool, slot_ids,
+                       True)

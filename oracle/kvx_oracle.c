@@ -220,3 +220,79 @@ int oracle_unpack(const oracle_layout *lay, int block_order, uint8_t *const *lay
     return oracle_run(lay, block_order, layer_ptrs, num_blocks, block_stride, block_table,
                       n_tokens, (uint8_t *)pool, num_slots, chunk_ids, nthreads, 0);
 }
+
+/* ---- Recurrent-state snapshot pages (Sec. 2.2) ---------------------------------- */
+
+int oracle_state_validate(int64_t num_layers, int64_t page_bytes, int64_t page_stride, int64_t num_pages,
+                          const int64_t *pages, int64_t n, int64_t num_state_slots, const int64_t *slot_ids,
+                          int for_pack)
+{
+    if (num_layers < 1 || page_bytes < 1 || page_stride < page_bytes || num_pages < 1 || n < 0 ||
+        num_state_slots < 0)
+        return ORACLE_EINVAL;
+    if (n == 0)
+        return ORACLE_OK;
+    if (!pages || !slot_ids)
+        return ORACLE_EINVAL;
+    for (int64_t k = 0; k < n; ++k) {
+        if (pages[k] < 0 || pages[k] >= num_pages)
+            return ORACLE_EINVAL;
+        if (slot_ids[k] < 0 || slot_ids[k] >= num_state_slots)
+            return ORACLE_EINVAL;
+    }
+    /* The side written must not be named twice. */
+    const int64_t *written = for_pack ? slot_ids : pages;
+    for (int64_t k = 0; k < n; ++k)
+        for (int64_t m = k + 1; m < n; ++m)
+            if (written[k] == written[m])
+                return ORACLE_EINVAL;
+    return ORACLE_OK;
+}
+
+static int oracle_state_run(int64_t num_layers, int64_t page_bytes, int64_t page_stride, int64_t num_pages,
+                            uint8_t *const *state_layers, const int64_t *pages, int64_t n, uint8_t *state_pool,
+                            int64_t num_state_slots, const int64_t *slot_ids, int to_pool)
+{
+    int rc = oracle_state_validate(num_layers, page_bytes, page_stride, num_pages, pages, n, num_state_slots,
+                                   slot_ids, to_pool);
+    if (rc != ORACLE_OK)
+        return rc;
+    if (n == 0)
+        return ORACLE_OK;
+    if (!state_layers || !state_pool)
+        return ORACLE_EINVAL;
+    for (int64_t g = 0; g < num_layers; ++g)
+        if (!state_layers[g])
+            return ORACLE_EINVAL;
+    int64_t snapshot_bytes = num_layers * page_bytes;
+    for (int64_t k = 0; k < n; ++k) {
+        uint8_t *slot = state_pool + slot_ids[k] * snapshot_bytes;
+        for (int64_t g = 0; g < num_layers; ++g) {
+            uint8_t *page = state_layers[g] + pages[k] * page_stride;
+            uint8_t *packed = slot + g * page_bytes;
+            if (to_pool)
+                memcpy(packed, page, (size_t)page_bytes);
+            else
+                memcpy(page, packed, (size_t)page_bytes);
+        }
+    }
+    return ORACLE_OK;
+}
+
+int oracle_state_pack(int64_t num_layers, int64_t page_bytes, int64_t page_stride, int64_t num_pages,
+                      const uint8_t *const *state_layers, const int64_t *pages, int64_t n,
+                      uint8_t *state_pool, int64_t num_state_slots, const int64_t *slot_ids)
+{
+    /* The pages are only read in this direction. */
+    return oracle_state_run(num_layers, page_bytes, page_stride, num_pages, (uint8_t *const *)state_layers,
+                            pages, n, state_pool, num_state_slots, slot_ids, 1);
+}
+
+int oracle_state_unpack(int64_t num_layers, int64_t page_bytes, int64_t page_stride, int64_t num_pages,
+                        uint8_t *const *state_layers, const int64_t *pages, int64_t n,
+                        const uint8_t *state_pool, int64_t num_state_slots, const int64_t *slot_ids)
+{
+    /* The state pool is only read in this direction. */
+    return oracle_state_run(num_layers, page_bytes, page_stride, num_pages, state_layers, pages, n,
+                            (uint8_t *)state_pool, num_state_slots, slot_ids, 0);
+}

@@ -82,6 +82,32 @@ int oracle_unpack(const oracle_layout *lay, int block_order, uint8_t *const *lay
                   int64_t n_tokens, const uint8_t *pool, int64_t num_slots,
                   const int64_t *chunk_ids, int nthreads);
 
+/*
+ * Recurrent-state snapshot pages of a hybrid model (Sec. 2.2): each of G recurrent
+ * layers keeps its boundary snapshot -- convolution state, recurrent state and
+ * padding -- as one page of page_bytes opaque bytes.  Layer g's page p sits at
+ * state_layers[g] + p*page_stride.  Snapshot k (pages[k] in every layer) is stored
+ * in state slot slot_ids[k] of a state pool of state slots G*page_bytes bytes each,
+ * layer-major: layer g's page at byte g*page_bytes of the slot.  Unpack is the
+ * exact inverse; no other byte of either side is touched.
+ *
+ * Validation: G >= 1, page_bytes >= 1, page_stride >= page_bytes, num_pages >= 1,
+ * n >= 0, every page id in [0, num_pages), every slot id in [0, num_state_slots);
+ * pack: slot ids pairwise distinct; unpack: page ids pairwise distinct (either
+ * repetition would make the result depend on the copy order).
+ */
+int oracle_state_validate(int64_t num_layers, int64_t page_bytes, int64_t page_stride, int64_t num_pages,
+                          const int64_t *pages, int64_t n, int64_t num_state_slots, const int64_t *slot_ids,
+                          int for_pack);
+
+int oracle_state_pack(int64_t num_layers, int64_t page_bytes, int64_t page_stride, int64_t num_pages,
+                      const uint8_t *const *state_layers, const int64_t *pages, int64_t n,
+                      uint8_t *state_pool, int64_t num_state_slots, const int64_t *slot_ids);
+
+int oracle_state_unpack(int64_t num_layers, int64_t page_bytes, int64_t page_stride, int64_t num_pages,
+                        uint8_t *const *state_layers, const int64_t *pages, int64_t n,
+                        const uint8_t *state_pool, int64_t num_state_slots, const int64_t *slot_ids);
+
 #ifdef __cplusplus
 }
 #endif

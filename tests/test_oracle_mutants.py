@@ -29,6 +29,15 @@ MUTANTS = {
                               "return b * block_stride + ((kv * BS + s) * H + h) * row_bytes;"),
     "nhd_read_as_hnd": ("return b * block_stride + ((kv * BS + s) * H + h) * row_bytes;",
                         "return b * block_stride + ((kv * H + h) * BS + s) * row_bytes;"),
+    "state_layer_offset_dropped": ("uint8_t *packed = slot + g * page_bytes;", "uint8_t *packed = slot;"),
+    "state_page_stride_ignored": ("state_layers[g] + pages[k] * page_stride;",
+                                  "state_layers[g] + pages[k] * page_bytes;"),
+    "state_slot_stride_one_page": ("state_pool + slot_ids[k] * snapshot_bytes;",
+                                   "state_pool + slot_ids[k] * page_bytes;"),
+    "state_unpack_wrong_way": ("memcpy(page, packed, (size_t)page_bytes);",
+                               "memcpy(packed, page, (size_t)page_bytes);"),
+    "state_duplicate_check_one_side": ("const int64_t *written = for_pack ? slot_ids : pages;",
+                                       "const int64_t *written = slot_ids;"),
 }
 
 
@@ -45,6 +54,7 @@ def test_pins_catch_mutant(name, tmp_path):
     env = dict(os.environ, KVX_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_nhd.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_nhd.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_state.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"

@@ -38,6 +38,17 @@
  *    kv_load.  The layout is fixed by this descriptor, never inferred from a
  *    tensor's rank or shape (the representation fault of Sec. 3.1).
  *
+ *  State snapshots (hybrid models, Sec. 2.2): each of G recurrent layers keeps
+ *    its boundary snapshot -- convolution state, recurrent state and padding --
+ *    as one page of page_bytes opaque bytes; layer g's page p sits at
+ *    layer_ptrs[g] + p*page_stride on the device.  Snapshot k of a request
+ *    (page pages[k] of every layer) is stored in state slot slot_ids[k] of the
+ *    pool's state area, layer-major [G][page_bytes]: layer g's page at byte
+ *    g*page_bytes of the slot.  A state slot is G*page_bytes bytes.  Under
+ *    aligned recovery (Sec. 2.2) a prefix is restorable only where both its
+ *    chunks and the snapshot at its boundary were stored; the two transfers are
+ *    separate calls ordered on one stream.
+ *
  * Ordering contract (Sec. 3.2 and Fig. 2):
  *  (i)   every device read (store) or write (load) of the cache, and every pool
  *        access, happens after all work enqueued on `stream` before the call;
@@ -122,6 +133,8 @@ typedef struct kv_pool_options {
                                   staged, 256 zero-copy); applies to the mode given here */
     int32_t side_streams;      /* staged: DMA side streams, 1..8 (default 2) */
     int32_t profile;           /* nonzero: time every pack/unpack launch (kv_pool_kernel_stats) */
+    int64_t num_state_slots;   /* state-snapshot slots (0 = no state area) */
+    int64_t state_slot_bytes;  /* bytes of one state slot = G*page_bytes, a multiple of 16 (0 if none) */
 } kv_pool_options;
 
 typedef struct kv_pool kv_pool;
@@ -142,7 +155,21 @@ typedef struct kv_pool_info {
     int32_t staging_contiguous; /* 1: staging is one physically contiguous device allocation */
     void *host_base;           /* host address of slot 0 */
     void *device_base;         /* device address of slot 0 (mapped pinned memory) */
+    int64_t num_state_slots;
+    int64_t state_slot_bytes;
+    void *state_host_base;     /* host address of state slot 0 (NULL without a state area); the
+                                  state area follows the chunk slots in the same pinned region */
 } kv_pool_info;
+
+/* A replica's recurrent-state page buffers (hybrid models).  The caller owns all memory. */
+typedef struct kv_state {
+    int32_t num_layers;        /* G >= 1 recurrent layers */
+    int32_t device;            /* HIP device ordinal the buffers live on */
+    int64_t page_bytes;        /* bytes of one layer's snapshot page (opaque) */
+    int64_t page_stride;       /* bytes between pages in a layer buffer; 0 = page_bytes */
+    int64_t num_pages;         /* pages per layer buffer */
+    void *const *layer_ptrs;   /* HOST array of G DEVICE pointers, read during the call only */
+} kv_state;
 
 /*
  * kv_pool_create -- allocate the shared host tier (Sec. 2: a host-RAM pool
@@ -166,6 +193,9 @@ KV_API kv_status kv_pool_destroy(kv_pool *pool);
 /* Fills *info.  KV_EINVAL on NULL arguments. */
 KV_API kv_status kv_pool_get_info(const kv_pool *pool, kv_pool_info *info);
 
+/* Host address of state slot `slot` (NULL if out of range or without a state area). */
+KV_API void *kv_pool_state_slot(kv_pool *pool, int64_t slot);
+
 /* Host address of a slot (NULL if out of range).  Touch it only when no call using it is in flight. */
 KV_API void *kv_pool_slot(kv_pool *pool, int64_t slot);
 KV_API int64_t kv_pool_slot_bytes(const kv_pool *pool);  /* -1 on NULL */
@@ -183,7 +213,7 @@ KV_API kv_status kv_pool_set_mode(kv_pool *pool, uint32_t mode);
 KV_API int32_t kv_pool_async_error(kv_pool *pool, int clear);
 
 /*
- * Accumulated pack (which = 0) or unpack (which = 1) kernel time of a pool
+ * Accumulated pack (which = 0), unpack (1), state pack (2) or state unpack (3) kernel time of a pool
  * created with opts.profile != 0.  Call after synchronising the streams used;
  * each launch's start/end events were recorded on the caller stream around it.
  * *launches, *total_ms and *bytes (algorithmic bytes: payload read + written)
@@ -235,6 +265,38 @@ KV_API kv_status kv_store(const kv_cache *cache, const int32_t *block_table, int
  */
 KV_API kv_status kv_load(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, kv_pool *pool,
                   const int64_t *chunk_ids, void *stream);
+
+/*
+ * Host-only validation of a state-snapshot request, no HIP call.  Checks:
+ * G >= 1; page_bytes >= 1; page_stride 0 or >= page_bytes; num_pages >= 1;
+ * G*page_bytes == pool_state_slot_bytes (the pool's snapshot format); n >= 0;
+ * for n > 0 non-NULL layer pointers, pages and slot_ids, page ids in
+ * [0, num_pages), slot ids in [0, pool_state_slots); a store's slot ids and a
+ * load's page ids pairwise distinct (the written side named twice would make
+ * the result order dependent).  GPU-path limits give KV_EUNSUPPORTED: G > 64,
+ * page_bytes, page_stride or a layer pointer not a multiple of 16.
+ */
+KV_API kv_status kv_check_state(const kv_state *state, int64_t pool_state_slot_bytes, int64_t pool_state_slots,
+                                int64_t n, const int64_t *pages, const int64_t *slot_ids, int for_store);
+
+/*
+ * kv_store_state -- store n recurrent-state snapshots (Sec. 2.2: the boundary
+ * snapshots of the recurrent layers, as opaque pages) into the pool's state
+ * area: page pages[k] of every layer into state slot slot_ids[k], in the
+ * state-slot format above.  The pool's mode applies (zero-copy kernels on
+ * `stream`, or packing into device staging plus DMA copies on the side streams,
+ * with the same ordering contract (i)-(iv) as kv_store).
+ *   pages, slot_ids: HOST int64[n], read before return.
+ * Enqueues only; n == 0 is a no-op; argument errors (kv_check_state) return
+ * before anything is enqueued; KV_EINVAL if the pool has no state area.
+ */
+KV_API kv_status kv_store_state(const kv_state *state, const int64_t *pages, int64_t n, kv_pool *pool,
+                                const int64_t *slot_ids, void *stream);
+
+/* kv_load_state -- the exact inverse: state slot slot_ids[k] into page pages[k] of every
+ * layer.  Writes only those pages' first page_bytes bytes.  As kv_store_state otherwise. */
+KV_API kv_status kv_load_state(const kv_state *state, const int64_t *pages, int64_t n, kv_pool *pool,
+                               const int64_t *slot_ids, void *stream);
 
 /* Thread-local text of the last failure on this thread (HIP error name, message, call site). */
 KV_API const char *kv_last_error(void);

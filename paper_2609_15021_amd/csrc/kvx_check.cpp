@@ -138,6 +138,66 @@ kv_status check_request(const kv_cache *cache, const kv_layout *pool_layout, int
     return KV_OK;
 }
 
+kv_status check_state_request(const kv_state *state, int64_t pool_state_slot_bytes, int64_t pool_state_slots,
+                              int64_t n, const int64_t *pages, const int64_t *slot_ids, int for_store) {
+    if (!state)
+        return fail(KV_EINVAL, "state must not be NULL");
+    const int64_t G = state->num_layers, pb = state->page_bytes;
+    const int64_t stride = state->page_stride ? state->page_stride : pb;
+    if (G < 1)
+        return fail(KV_EINVAL, "state num_layers must be >= 1 (got %lld)", static_cast<long long>(G));
+    if (pb < 1)
+        return fail(KV_EINVAL, "page_bytes must be >= 1 (got %lld)", static_cast<long long>(pb));
+    if (stride < pb)
+        return fail(KV_EINVAL, "page_stride %lld is smaller than page_bytes %lld", static_cast<long long>(stride),
+                    static_cast<long long>(pb));
+    if (state->num_pages < 1)
+        return fail(KV_EINVAL, "num_pages must be >= 1 (got %lld)", static_cast<long long>(state->num_pages));
+    if (pb > INT64_MAX / G || G * pb != pool_state_slot_bytes)
+        return fail(KV_EINVAL, "snapshot of %lld layers x %lld bytes differs from the pool's state slot of %lld bytes",
+                    static_cast<long long>(G), static_cast<long long>(pb),
+                    static_cast<long long>(pool_state_slot_bytes));
+    if (G > kMaxStateLayers)
+        return fail(KV_EUNSUPPORTED, "more than %d recurrent layers", kMaxStateLayers);
+    if (pb % 16 != 0 || stride % 16 != 0)
+        return fail(KV_EUNSUPPORTED, "page_bytes %lld and page_stride %lld must be multiples of 16",
+                    static_cast<long long>(pb), static_cast<long long>(stride));
+    if (state->num_pages > INT64_MAX / stride)
+        return fail(KV_EUNSUPPORTED, "page buffer size overflows 64 bits");
+    if (n < 0)
+        return fail(KV_EINVAL, "n must be >= 0 (got %lld)", static_cast<long long>(n));
+    if (n == 0)
+        return KV_OK;
+    if (!state->layer_ptrs)
+        return fail(KV_EINVAL, "state layer_ptrs must not be NULL");
+    for (int64_t g = 0; g < G; ++g) {
+        const uintptr_t p = reinterpret_cast<uintptr_t>(state->layer_ptrs[g]);
+        if (p == 0)
+            return fail(KV_EINVAL, "state layer_ptrs[%lld] is NULL", static_cast<long long>(g));
+        if (p % 16 != 0)
+            return fail(KV_EUNSUPPORTED, "state layer_ptrs[%lld] is not 16-byte aligned", static_cast<long long>(g));
+    }
+    if (!pages || !slot_ids)
+        return fail(KV_EINVAL, "pages and slot_ids must not be NULL for n > 0");
+    for (int64_t k = 0; k < n; ++k) {
+        if (pages[k] < 0 || pages[k] >= state->num_pages)
+            return fail(KV_EINVAL, "pages[%lld] = %lld is outside [0, %lld)", static_cast<long long>(k),
+                        static_cast<long long>(pages[k]), static_cast<long long>(state->num_pages));
+        if (slot_ids[k] < 0 || slot_ids[k] >= pool_state_slots)
+            return fail(KV_EINVAL, "slot_ids[%lld] = %lld is outside [0, %lld)", static_cast<long long>(k),
+                        static_cast<long long>(slot_ids[k]), static_cast<long long>(pool_state_slots));
+    }
+    // The side this call writes must not be named twice.
+    const int64_t *written = for_store ? slot_ids : pages;
+    std::unordered_set<int64_t> seen;
+    seen.reserve(static_cast<size_t>(n) * 2);
+    for (int64_t k = 0; k < n; ++k)
+        if (!seen.insert(written[k]).second)
+            return fail(KV_EINVAL, "%s %lld appears twice in one %s", for_store ? "state slot" : "page",
+                        static_cast<long long>(written[k]), for_store ? "store" : "load");
+    return KV_OK;
+}
+
 }  // namespace kvx
 
 extern "C" {
@@ -168,6 +228,11 @@ const char *kv_version(void) { return "kvx 0.1.0 (gfx950)"; }
 kv_status kv_check(const kv_cache *cache, const kv_layout *pool_layout, int64_t pool_slots, int64_t n_tokens,
                    const int64_t *chunk_ids, int for_store) {
     return kvx::check_request(cache, pool_layout, pool_slots, n_tokens, chunk_ids, for_store);
+}
+
+kv_status kv_check_state(const kv_state *state, int64_t pool_state_slot_bytes, int64_t pool_state_slots, int64_t n,
+                         const int64_t *pages, const int64_t *slot_ids, int for_store) {
+    return kvx::check_state_request(state, pool_state_slot_bytes, pool_state_slots, n, pages, slot_ids, for_store);
 }
 
 }  // extern "C"

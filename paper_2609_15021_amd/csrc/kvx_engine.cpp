@@ -14,8 +14,10 @@
 //    completed -- premature reuse of an asynchronous-copy buffer is the related failure
 //    the paper cites (Sec. 3.2).
 // No call ever blocks the host on device work.
+#include <algorithm>
 #include <chrono>
 #include <cstring>
+#include <functional>
 
 #include "kvx_internal.h"
 
@@ -49,7 +51,7 @@ kv_status release(kv_pool *p) {
             note(hipEventDestroy(e), "hipEventDestroy");
     if (p->ev_entry)
         note(hipEventDestroy(p->ev_entry), "hipEventDestroy");
-    for (int w = 0; w < 2; ++w)
+    for (int w = 0; w < 4; ++w)
         for (auto &t : p->pending[w]) {
             note(hipEventSynchronize(t.stop), "hipEventSynchronize");
             note(hipEventDestroy(t.start), "hipEventDestroy");
@@ -81,13 +83,13 @@ kv_status take_timing_event(kv_pool *p, hipEvent_t *e) {
     return make_event(e, true);
 }
 
-// Check the current device and the cache's device against the pool's.
-kv_status check_device(const kv_pool *p, const kv_cache *cache) {
+// Check the current device and the buffers' device against the pool's.
+kv_status check_device(const kv_pool *p, int buffers_device) {
     int cur = -1;
     KVX_HIP(hipGetDevice(&cur));
-    if (cur != p->device || cache->device != p->device)
-        return kvx::fail(KV_EINVAL, "pool is on device %d, cache on device %d, current device %d", p->device,
-                         cache->device, cur);
+    if (cur != p->device || buffers_device != p->device)
+        return kvx::fail(KV_EINVAL, "pool is on device %d, buffers on device %d, current device %d", p->device,
+                         buffers_device, cur);
     return KV_OK;
 }
 
@@ -153,34 +155,94 @@ kv_status enqueue_gather(kv_pool *p, const kv_cache *cache, const int32_t *block
     return KV_OK;
 }
 
-// Contiguous host<->staging copy runs of one staged batch: consecutive chunks whose slots
-// are consecutive and whose earlier members are full merge into one DMA copy.
-struct CopyRun {
-    int64_t first_chunk;  // index within the batch
-    int64_t slot;         // pool slot of the first chunk
+// One DMA copy of a staged batch: host_base + host_off <-> staging slot + stage_off.
+struct Run {
+    int64_t host_off;
+    int64_t stage_off;
     int64_t bytes;
 };
 
-std::vector<CopyRun> copy_runs(const kv_pool *p, int64_t n_tokens, int64_t chunk0, int nchunks,
-                               const int64_t *chunk_ids) {
-    std::vector<CopyRun> runs;
-    const Geometry &g = p->geo;
-    for (int c = 0; c < nchunks; ++c) {
-        const int64_t i = chunk0 + c;
-        const int64_t r = std::min<int64_t>(g.C, n_tokens - i * g.C);
-        const int64_t bytes = r * g.token_bytes;
-        if (!runs.empty()) {
-            CopyRun &last = runs.back();
-            const int64_t members = c - last.first_chunk;
-            const bool prev_full = last.bytes == members * g.slot_bytes;
-            if (prev_full && chunk_ids[i] == last.slot + members) {
-                last.bytes += bytes;
-                continue;
-            }
+// Append a copy, merging it into the previous one when both sides are contiguous.
+void add_run(std::vector<Run> &runs, int64_t host_off, int64_t stage_off, int64_t bytes) {
+    if (!runs.empty()) {
+        Run &last = runs.back();
+        if (last.host_off + last.bytes == host_off && last.stage_off + last.bytes == stage_off) {
+            last.bytes += bytes;
+            return;
         }
-        runs.push_back({c, chunk_ids[i], bytes});
     }
-    return runs;
+    runs.push_back({host_off, stage_off, bytes});
+}
+
+using BatchRuns = std::function<void(int64_t batch, std::vector<Run> &runs)>;
+using BatchKernels = std::function<kv_status(int64_t batch, uint8_t *stage)>;
+
+// The staged pipeline over `nbatches` batches, each filling at most one staging slot.
+// Store: kernels on the caller's stream pack batch b into staging slot k (after the copy
+// that last read slot k), then a side stream copies it to the pool; the caller's stream
+// finally waits for every side stream (exit join).  Load: an entry event on the caller's
+// stream gates the side streams' pool reads; each batch's kernels wait for its copy.
+kv_status staged_pipeline(kv_pool *p, int64_t nbatches, const BatchRuns &runs_of, const BatchKernels &kernels,
+                          hipStream_t stream, Direction dir) {
+    const int64_t staging_slot_bytes = static_cast<int64_t>(p->cpb) * p->geo.slot_bytes;
+    std::vector<bool> side_used(p->sides.size(), false);
+    std::vector<Run> runs;
+
+    if (dir == kvx::kUnpack)
+        KVX_HIP(hipEventRecord(p->ev_entry, stream));  // entry gate for pool reads
+
+    for (int64_t b = 0; b < nbatches; ++b) {
+        const int k = p->ring;
+        p->ring = (p->ring + 1) % p->K;
+        const size_t si = static_cast<size_t>(b % static_cast<int64_t>(p->sides.size()));
+        hipStream_t side = p->sides[si];
+        uint8_t *stage = p->staging + static_cast<int64_t>(k) * staging_slot_bytes;
+        runs.clear();
+        runs_of(b, runs);
+
+        if (dir == kvx::kPack) {
+            if (p->free_recorded[k])
+                KVX_HIP(hipStreamWaitEvent(stream, p->ev_free[k], 0));
+            kv_status st = kernels(b, stage);
+            if (st != KV_OK)
+                return st;
+            KVX_HIP(hipEventRecord(p->ev_ready[k], stream));
+            KVX_HIP(hipStreamWaitEvent(side, p->ev_ready[k], 0));
+            for (const Run &run : runs)
+                KVX_HIP(hipMemcpyAsync(p->host_base + run.host_off, stage + run.stage_off,
+                                       static_cast<size_t>(run.bytes), hipMemcpyDeviceToHost, side));
+            KVX_HIP(hipEventRecord(p->ev_free[k], side));
+            p->free_recorded[k] = true;
+            side_used[si] = true;
+        } else {
+            if (!side_used[si]) {
+                KVX_HIP(hipStreamWaitEvent(side, p->ev_entry, 0));
+                side_used[si] = true;
+            }
+            if (p->free_recorded[k])
+                KVX_HIP(hipStreamWaitEvent(side, p->ev_free[k], 0));
+            for (const Run &run : runs)
+                KVX_HIP(hipMemcpyAsync(stage + run.stage_off, p->host_base + run.host_off,
+                                       static_cast<size_t>(run.bytes), hipMemcpyHostToDevice, side));
+            KVX_HIP(hipEventRecord(p->ev_ready[k], side));
+            KVX_HIP(hipStreamWaitEvent(stream, p->ev_ready[k], 0));
+            kv_status st = kernels(b, stage);
+            if (st != KV_OK)
+                return st;
+            KVX_HIP(hipEventRecord(p->ev_free[k], stream));
+            p->free_recorded[k] = true;
+        }
+    }
+    if (dir == kvx::kPack) {
+        // Exit join: later work on the caller's stream follows every D2H copy.
+        for (size_t si = 0; si < p->sides.size(); ++si) {
+            if (!side_used[si])
+                continue;
+            KVX_HIP(hipEventRecord(p->ev_join[si], p->sides[si]));
+            KVX_HIP(hipStreamWaitEvent(stream, p->ev_join[si], 0));
+        }
+    }
+    return KV_OK;
 }
 
 kv_status transfer(kv_pool *p, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
@@ -202,71 +264,135 @@ kv_status transfer(kv_pool *p, const kv_cache *cache, const int32_t *block_table
         return KV_OK;
     }
 
-    // Staged mode.
+    // Staged mode: batch b holds chunks [b*cpb, b*cpb + cpb) in staging slots 0..cpb-1.
     std::vector<int32_t> local(static_cast<size_t>(p->cpb));
     for (int c = 0; c < p->cpb; ++c)
         local[static_cast<size_t>(c)] = c;
-    const int64_t staging_slot_bytes = static_cast<int64_t>(p->cpb) * g.slot_bytes;
-    std::vector<bool> side_used(p->sides.size(), false);
-
-    if (dir == kvx::kUnpack)
-        KVX_HIP(hipEventRecord(p->ev_entry, stream));  // entry gate for pool reads
-
-    int64_t batch = 0;
-    for (int64_t c0 = 0; c0 < nc; c0 += p->cpb, ++batch) {
+    const int64_t nbatches = (nc + p->cpb - 1) / p->cpb;
+    auto runs_of = [&](int64_t b, std::vector<Run> &runs) {
+        const int64_t c0 = b * p->cpb;
+        const int64_t n = std::min<int64_t>(p->cpb, nc - c0);
+        for (int64_t c = 0; c < n; ++c) {
+            const int64_t i = c0 + c;
+            const int64_t r = std::min<int64_t>(g.C, n_tokens - i * g.C);
+            add_run(runs, chunk_ids[i] * g.slot_bytes, c * g.slot_bytes, r * g.token_bytes);
+        }
+    };
+    auto kernels = [&](int64_t b, uint8_t *stage) {
+        const int64_t c0 = b * p->cpb;
         const int n = static_cast<int>(std::min<int64_t>(p->cpb, nc - c0));
-        const int k = p->ring;
-        p->ring = (p->ring + 1) % p->K;
-        const size_t si = static_cast<size_t>(batch % static_cast<int64_t>(p->sides.size()));
-        hipStream_t side = p->sides[si];
-        uint8_t *stage = p->staging + static_cast<int64_t>(k) * staging_slot_bytes;
-        const std::vector<CopyRun> runs = copy_runs(p, n_tokens, c0, n, chunk_ids);
+        return enqueue_gather(p, cache, block_table, n_tokens, dir, c0, n, local.data(), stage, g.slot_bytes,
+                              false, stream);
+    };
+    return staged_pipeline(p, nbatches, runs_of, kernels, stream, dir);
+}
 
-        if (dir == kvx::kPack) {
-            if (p->free_recorded[k])
-                KVX_HIP(hipStreamWaitEvent(stream, p->ev_free[k], 0));
-            kv_status st = enqueue_gather(p, cache, block_table, n_tokens, dir, c0, n, local.data(), stage,
-                                          g.slot_bytes, false, stream);
-            if (st != KV_OK)
-                return st;
-            KVX_HIP(hipEventRecord(p->ev_ready[k], stream));
-            KVX_HIP(hipStreamWaitEvent(side, p->ev_ready[k], 0));
-            for (const CopyRun &run : runs)
-                KVX_HIP(hipMemcpyAsync(p->host_base + run.slot * g.slot_bytes, stage + run.first_chunk * g.slot_bytes,
-                                       static_cast<size_t>(run.bytes), hipMemcpyDeviceToHost, side));
-            KVX_HIP(hipEventRecord(p->ev_free[k], side));
-            p->free_recorded[k] = true;
-            side_used[si] = true;
-        } else {
-            if (!side_used[si]) {
-                KVX_HIP(hipStreamWaitEvent(side, p->ev_entry, 0));
-                side_used[si] = true;
-            }
-            if (p->free_recorded[k])
-                KVX_HIP(hipStreamWaitEvent(side, p->ev_free[k], 0));
-            for (const CopyRun &run : runs)
-                KVX_HIP(hipMemcpyAsync(stage + run.first_chunk * g.slot_bytes, p->host_base + run.slot * g.slot_bytes,
-                                       static_cast<size_t>(run.bytes), hipMemcpyHostToDevice, side));
-            KVX_HIP(hipEventRecord(p->ev_ready[k], side));
-            KVX_HIP(hipStreamWaitEvent(stream, p->ev_ready[k], 0));
-            kv_status st = enqueue_gather(p, cache, block_table, n_tokens, dir, c0, n, local.data(), stage,
-                                          g.slot_bytes, false, stream);
-            if (st != KV_OK)
-                return st;
-            KVX_HIP(hipEventRecord(p->ev_free[k], stream));
-            p->free_recorded[k] = true;
-        }
+// Piece arithmetic of one state request: n snapshots of G pages, each page cut into
+// ppp pieces of `piece` bytes (the last piece of a page may be shorter).  Piece q is
+// piece j of layer g of snapshot k with q = (k*G + g)*ppp + j; its packed bytes start
+// at off(q) in the concatenation of the n packed snapshots.
+struct StatePlan {
+    int64_t n, G, page_bytes, page_stride, snap_bytes, piece, ppp, pieces;
+
+    StatePlan(const kv_state *st, int64_t n_snap, int64_t piece_bytes)
+        : n(n_snap), G(st->num_layers), page_bytes(st->page_bytes),
+          page_stride(st->page_stride ? st->page_stride : st->page_bytes), snap_bytes(G * page_bytes),
+          piece(std::min(piece_bytes, page_bytes)), ppp((page_bytes + piece - 1) / piece), pieces(n * G * ppp) {}
+
+    int64_t off(int64_t q) const {
+        const int64_t per = G * ppp;
+        const int64_t k = q / per, rem = q - k * per;
+        const int64_t g = rem / ppp, j = rem - g * ppp;
+        return k * snap_bytes + g * page_bytes + j * piece;
     }
-    if (dir == kvx::kPack) {
-        // Exit join: later work on the caller's stream follows every D2H copy.
-        for (size_t si = 0; si < p->sides.size(); ++si) {
-            if (!side_used[si])
-                continue;
-            KVX_HIP(hipEventRecord(p->ev_join[si], p->sides[si]));
-            KVX_HIP(hipStreamWaitEvent(stream, p->ev_join[si], 0));
+};
+
+// Enqueue the state kernels for pieces [qa, qb) on `stream`.  base: device-visible packed
+// side; snap_off(k): byte offset at base where snapshot k's packed bytes start.
+kv_status enqueue_state(kv_pool *p, const kv_state *st, const StatePlan &plan, const int64_t *pages, int64_t qa,
+                        int64_t qb, uint8_t *base, const std::function<int64_t(int64_t)> &snap_off, bool host_side,
+                        hipStream_t stream, Direction dir) {
+    hipEvent_t t_start = nullptr, t_stop = nullptr;
+    if (p->profile) {
+        kv_status e = take_timing_event(p, &t_start);
+        if (e != KV_OK)
+            return e;
+        e = take_timing_event(p, &t_stop);
+        if (e != KV_OK)
+            return e;
+        KVX_HIP(hipEventRecord(t_start, stream));
+    }
+    const int64_t per = plan.G * plan.ppp;
+    for (int64_t q = qa; q < qb;) {
+        const int64_t k_first = q / per;
+        const int64_t q_end = std::min({qb, q + kvx::kMaxLaunchPieces, (k_first + kvx::kMaxLaunchSnapshots) * per});
+        const int64_t k_last = (q_end - 1) / per;
+        kvx::StateArgs a;
+        std::memset(&a, 0, sizeof(a));
+        for (int64_t g = 0; g < plan.G; ++g)
+            a.layer[g] = static_cast<uint8_t *>(st->layer_ptrs[g]);
+        a.base = base;
+        a.page_stride = plan.page_stride;
+        a.page_bytes = plan.page_bytes;
+        a.piece = plan.piece;
+        a.q0 = q - k_first * per;
+        a.G = static_cast<int32_t>(plan.G);
+        a.ppp = static_cast<int32_t>(plan.ppp);
+        a.nsnap = static_cast<int32_t>(k_last - k_first + 1);
+        for (int64_t k = k_first; k <= k_last; ++k) {
+            a.page[k - k_first] = pages[k];
+            a.off[k - k_first] = snap_off(k);
         }
+        KVX_HIP(kvx::launch_state(a, q_end - q, dir, host_side, stream));
+        q = q_end;
+    }
+    if (p->profile) {
+        KVX_HIP(hipEventRecord(t_stop, stream));
+        p->pending[2 + dir].push_back({t_start, t_stop, 2.0 * static_cast<double>(plan.off(qb) - plan.off(qa))});
     }
     return KV_OK;
+}
+
+kv_status transfer_state(kv_pool *p, const kv_state *st, const int64_t *pages, int64_t n, const int64_t *slot_ids,
+                         hipStream_t stream, Direction dir) {
+    const int64_t S = p->state_slot_bytes;
+    if (p->mode == KV_MODE_ZERO_COPY) {
+        const StatePlan plan(st, n, kvx::kStatePiece);
+        auto off = [&](int64_t k) { return slot_ids[k] * S; };
+        return enqueue_state(p, st, plan, pages, 0, plan.pieces, p->dev_base + p->state_offset, off, true, stream,
+                             dir);
+    }
+
+    // Staged mode: cut the pieces into batches of at most one staging slot of bytes.
+    const int64_t cap = static_cast<int64_t>(p->cpb) * p->geo.slot_bytes;
+    const StatePlan plan(st, n, std::min<int64_t>(kvx::kStatePiece, cap / 16 * 16));
+    std::vector<int64_t> cut{0};
+    while (cut.back() < plan.pieces) {
+        const int64_t qa = cut.back(), oa = plan.off(qa);
+        int64_t lo = qa + 1, hi = plan.pieces;  // a single piece always fits
+        while (lo < hi) {
+            const int64_t mid = lo + (hi - lo + 1) / 2;
+            if (plan.off(mid) - oa <= cap)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        cut.push_back(lo);
+    }
+    const int64_t nbatches = static_cast<int64_t>(cut.size()) - 1;
+    auto runs_of = [&](int64_t b, std::vector<Run> &runs) {
+        const int64_t oa = plan.off(cut[b]), ob = plan.off(cut[b + 1]);
+        for (int64_t k = oa / S; k * S < ob; ++k) {
+            const int64_t lo = std::max(oa, k * S), hi = std::min(ob, (k + 1) * S);
+            add_run(runs, p->state_offset + slot_ids[k] * S + (lo - k * S), lo - oa, hi - lo);
+        }
+    };
+    auto kernels = [&](int64_t b, uint8_t *stage) {
+        const int64_t oa = plan.off(cut[b]);
+        auto off = [&](int64_t k) { return k * S - oa; };
+        return enqueue_state(p, st, plan, pages, cut[b], cut[b + 1], stage, off, false, stream, dir);
+    };
+    return staged_pipeline(p, nbatches, runs_of, kernels, stream, dir);
 }
 
 // Record the pool's last use on `stream` (one event per stream seen).
@@ -298,12 +424,34 @@ kv_status run(const kv_cache *cache, const int32_t *block_table, int64_t n_token
         return KV_OK;
     if (!block_table)
         return kvx::fail(KV_EINVAL, "block_table must not be NULL for n_tokens > 0");
-    st = check_device(pool, cache);
+    st = check_device(pool, cache->device);
     if (st != KV_OK)
         return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     st = transfer(pool, cache, block_table, n_tokens, chunk_ids, s, dir);
     // Record the last use on this stream even after a partial enqueue.
+    const kv_status st_use = mark_use(pool, s);
+    return st != KV_OK ? st : st_use;
+}
+
+kv_status run_state(const kv_state *state, const int64_t *pages, int64_t n, kv_pool *pool, const int64_t *slot_ids,
+                    void *stream, Direction dir) {
+    if (!pool)
+        return kvx::fail(KV_EINVAL, "pool must not be NULL");
+    std::lock_guard<std::mutex> lock(pool->mu);
+    if (pool->num_state_slots == 0)
+        return kvx::fail(KV_EINVAL, "pool was created without a state area (num_state_slots = 0)");
+    kv_status st = kvx::check_state_request(state, pool->state_slot_bytes, pool->num_state_slots, n, pages, slot_ids,
+                                            dir == kvx::kPack);
+    if (st != KV_OK)
+        return st;
+    if (n == 0)
+        return KV_OK;
+    st = check_device(pool, state->device);
+    if (st != KV_OK)
+        return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = transfer_state(pool, state, pages, n, slot_ids, s, dir);
     const kv_status st_use = mark_use(pool, s);
     return st != KV_OK ? st : st_use;
 }
@@ -339,6 +487,13 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
     const int S = opts->side_streams ? opts->side_streams : kDefaultSideStreams;
     if (want_staging && (S < 1 || S > 8))
         return kvx::fail(KV_EINVAL, "side_streams must be in [1, 8] (got %d)", S);
+    if (opts->num_state_slots < 0 || opts->state_slot_bytes < 0 ||
+        (opts->num_state_slots > 0) != (opts->state_slot_bytes > 0))
+        return kvx::fail(KV_EINVAL, "num_state_slots (%lld) and state_slot_bytes (%lld) must both be 0 or both > 0",
+                         static_cast<long long>(opts->num_state_slots), static_cast<long long>(opts->state_slot_bytes));
+    if (opts->state_slot_bytes % 16 != 0)
+        return kvx::fail(KV_EUNSUPPORTED, "state_slot_bytes %lld is not a multiple of 16",
+                         static_cast<long long>(opts->state_slot_bytes));
 
     kv_pool *p = new kv_pool();
     p->layout = *layout;
@@ -349,6 +504,16 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
         return kvx::fail(KV_EINVAL, "pool size overflows 64 bits");
     }
     p->pool_bytes = num_slots * p->geo.slot_bytes;
+    // The state-snapshot area follows the chunk slots in the same region, 4 KiB aligned.
+    p->num_state_slots = opts->num_state_slots;
+    p->state_slot_bytes = opts->state_slot_bytes;
+    p->state_offset = (p->pool_bytes + 4095) / 4096 * 4096;
+    if (p->num_state_slots > 0 && p->state_slot_bytes > (INT64_MAX - p->state_offset) / p->num_state_slots) {
+        delete p;
+        return kvx::fail(KV_EINVAL, "pool size with the state area overflows 64 bits");
+    }
+    const int64_t region_bytes =
+        p->num_state_slots > 0 ? p->state_offset + p->num_state_slots * p->state_slot_bytes : p->pool_bytes;
     p->mode = opts->mode;
     p->host_kind = opts->host_kind;
     p->profile = opts->profile != 0;
@@ -366,17 +531,17 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
     if (e != hipSuccess)
         return bail(kvx::hip_fail(e, "hipGetDevice", __FILE__, __LINE__));
 
-    // One pinned, mapped region of exactly pool_bytes (Sec. 3.3: no rounding allocator,
+    // One pinned, mapped region of exactly region_bytes (Sec. 3.3: no rounding allocator,
     // and never a silent fallback to pageable memory).
     const unsigned flags = hipHostMallocMapped | hipHostMallocPortable |
                            (p->host_kind == KV_HOST_COHERENT ? hipHostMallocCoherent : hipHostMallocNonCoherent);
     const auto t0 = std::chrono::steady_clock::now();
     void *host = nullptr;
-    e = hipHostMalloc(&host, static_cast<size_t>(p->pool_bytes), flags);
+    e = hipHostMalloc(&host, static_cast<size_t>(region_bytes), flags);
     const auto t1 = std::chrono::steady_clock::now();
     if (e != hipSuccess || !host) {
         (void)hipGetLastError();
-        const long long want = static_cast<long long>(p->pool_bytes);
+        const long long want = static_cast<long long>(region_bytes);
         release(p);
         return kvx::fail(KV_ENOMEM, "pinned allocation of %lld bytes failed (%s); no pageable fallback", want,
                          hipGetErrorName(e));
@@ -476,7 +641,16 @@ kv_status kv_pool_get_info(const kv_pool *pool, kv_pool_info *info) {
     info->staging_contiguous = pool->staging_contiguous ? 1 : 0;
     info->host_base = pool->host_base;
     info->device_base = pool->dev_base;
+    info->num_state_slots = pool->num_state_slots;
+    info->state_slot_bytes = pool->state_slot_bytes;
+    info->state_host_base = pool->num_state_slots > 0 ? pool->host_base + pool->state_offset : nullptr;
     return KV_OK;
+}
+
+void *kv_pool_state_slot(kv_pool *pool, int64_t slot) {
+    if (!pool || slot < 0 || slot >= pool->num_state_slots)
+        return nullptr;
+    return pool->host_base + pool->state_offset + slot * pool->state_slot_bytes;
 }
 
 void *kv_pool_slot(kv_pool *pool, int64_t slot) {
@@ -513,8 +687,10 @@ int32_t kv_pool_async_error(kv_pool *pool, int clear) {
 
 kv_status kv_pool_kernel_stats(kv_pool *pool, int which, int reset, int64_t *launches, double *total_ms,
                                double *bytes) {
-    if (!pool || which < 0 || which > 1)
-        return kvx::fail(KV_EINVAL, "pool must not be NULL and which must be 0 (pack) or 1 (unpack)");
+    if (!pool || which < 0 || which > 3)
+        return kvx::fail(KV_EINVAL,
+                         "pool must not be NULL and which must be 0 (pack), 1 (unpack), 2 (state pack) or "
+                         "3 (state unpack)");
     std::lock_guard<std::mutex> lock(pool->mu);
     auto &pend = pool->pending[which];
     size_t done = 0;
@@ -556,6 +732,20 @@ kv_status kv_store(const kv_cache *cache, const int32_t *block_table, int64_t n_
 kv_status kv_load(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, kv_pool *pool,
                   const int64_t *chunk_ids, void *stream) {
     return run(cache, block_table, n_tokens, pool, chunk_ids, stream, kvx::kUnpack);
+}
+
+}  // extern "C"
+
+extern "C" {
+
+kv_status kv_store_state(const kv_state *state, const int64_t *pages, int64_t n, kv_pool *pool,
+                         const int64_t *slot_ids, void *stream) {
+    return run_state(state, pages, n, pool, slot_ids, stream, kvx::kPack);
+}
+
+kv_status kv_load_state(const kv_state *state, const int64_t *pages, int64_t n, kv_pool *pool,
+                        const int64_t *slot_ids, void *stream) {
+    return run_state(state, pages, n, pool, slot_ids, stream, kvx::kUnpack);
 }
 
 }  // extern "C"

@@ -18,6 +18,10 @@ namespace kvx {
 constexpr int kThreads = KVX_THREADS;  // work-items per workgroup (wave64s x 64)
 constexpr int kMaxLaunchLayers = 64;   // layer pointers carried in one launch's kernel arguments
 constexpr int kMaxLaunchChunks = 256;  // slot ids carried in one launch's kernel arguments
+constexpr int kMaxStateLayers = 64;    // recurrent layers of a state snapshot (one launch carries all)
+constexpr int kMaxLaunchSnapshots = 128;  // snapshots carried in one state launch's arguments
+constexpr int64_t kStatePiece = 64 * 1024;  // bytes of a page one workgroup moves (at most)
+constexpr int64_t kMaxLaunchPieces = int64_t(1) << 22;  // workgroups of one state launch
 
 // Derived sizes of a layout (all bytes, 64-bit).
 struct Geometry {
@@ -57,6 +61,23 @@ struct GatherArgs {
 
 enum Direction { kPack = 0, kUnpack = 1 };
 
+// Kernel arguments of one state-snapshot launch.  Pages are cut into pieces of `piece`
+// bytes (the last piece of a page may be shorter); piece q of the launch is piece
+// j = q % ppp of layer g = (q / ppp) % G of snapshot k = q / (G*ppp).  The launch covers
+// pieces [q0, q0 + gridDim.x) of snapshots 0..nsnap-1 of its own lists.
+struct StateArgs {
+    uint8_t *layer[kMaxStateLayers];   // device base of each recurrent layer's page buffer
+    uint8_t *base;                     // device-visible packed side (state pool or staging)
+    int64_t page_stride, page_bytes, piece;
+    int64_t q0;
+    int32_t G, ppp, nsnap, pad;
+    int64_t page[kMaxLaunchSnapshots];  // device page id of each snapshot
+    int64_t off[kMaxLaunchSnapshots];   // byte offset at `base` of each snapshot's packed bytes
+};
+
+hipError_t launch_state(const StateArgs &args, int64_t pieces, Direction dir, bool host_side,
+                        hipStream_t stream);
+
 // Enqueue one launch on `stream`; host_side: the chunk side is mapped pinned host memory.
 // Returns the launch error (hipSuccess on success).
 hipError_t launch_gather(const GatherArgs &args, Direction dir, bool host_side, hipStream_t stream);
@@ -80,6 +101,8 @@ void set_last_error(const std::string &msg);
 kv_status check_layout(const kv_layout &lay);
 kv_status check_request(const kv_cache *cache, const kv_layout *pool_layout, int64_t pool_slots,
                         int64_t n_tokens, const int64_t *chunk_ids, int for_store);
+kv_status check_state_request(const kv_state *state, int64_t pool_state_slot_bytes, int64_t pool_state_slots,
+                              int64_t n, const int64_t *pages, const int64_t *slot_ids, int for_store);
 
 }  // namespace kvx
 
@@ -88,6 +111,9 @@ struct kv_pool {
     kv_layout layout{};
     kvx::Geometry geo{};
     int64_t num_slots = 0, pool_bytes = 0;
+    // Recurrent-state snapshot area: num_state_slots slots of state_slot_bytes each, starting
+    // state_offset bytes into the pinned region (after the chunk slots).
+    int64_t num_state_slots = 0, state_slot_bytes = 0, state_offset = 0;
     int device = 0;
     uint32_t mode = 0, host_kind = 0;
     uint8_t *host_base = nullptr;   // host address of slot 0
@@ -113,17 +139,18 @@ struct kv_pool {
     // kv_pool_destroy never frees memory that queued kernels or copies still touch.
     std::vector<std::pair<hipStream_t, hipEvent_t>> last_use;
 
-    // Profiling of pack/unpack launches.
+    // Profiling of pack/unpack and state launches.
     bool profile = false;
     struct Timed {
         hipEvent_t start, stop;
         double bytes;
     };
-    std::vector<Timed> pending[2];
+    // Index: 0 pack, 1 unpack, 2 state pack, 3 state unpack.
+    std::vector<Timed> pending[4];
     std::vector<hipEvent_t> spare_events;
-    int64_t launches[2] = {0, 0};
-    double total_ms[2] = {0.0, 0.0};
-    double total_bytes[2] = {0.0, 0.0};
+    int64_t launches[4] = {0, 0, 0, 0};
+    double total_ms[4] = {0.0, 0.0, 0.0, 0.0};
+    double total_bytes[4] = {0.0, 0.0, 0.0, 0.0};
 
     std::mutex mu;
 };

@@ -52,7 +52,8 @@ class KvCache(ctypes.Structure):
 class KvPoolOptions(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_uint32), ("host_kind", ctypes.c_uint32),
                 ("staging_slots", ctypes.c_int32), ("chunks_per_batch", ctypes.c_int32),
-                ("side_streams", ctypes.c_int32), ("profile", ctypes.c_int32)]
+                ("side_streams", ctypes.c_int32), ("profile", ctypes.c_int32),
+                ("num_state_slots", ctypes.c_int64), ("state_slot_bytes", ctypes.c_int64)]
 
 
 class KvPoolInfo(ctypes.Structure):
@@ -63,7 +64,14 @@ class KvPoolInfo(ctypes.Structure):
                 ("is_pinned", ctypes.c_int32), ("staging_slots", ctypes.c_int32),
                 ("chunks_per_batch", ctypes.c_int32), ("side_streams", ctypes.c_int32),
                 ("staging_contiguous", ctypes.c_int32), ("host_base", ctypes.c_void_p),
-                ("device_base", ctypes.c_void_p)]
+                ("device_base", ctypes.c_void_p), ("num_state_slots", ctypes.c_int64),
+                ("state_slot_bytes", ctypes.c_int64), ("state_host_base", ctypes.c_void_p)]
+
+
+class KvState(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("device", ctypes.c_int32), ("page_bytes", ctypes.c_int64),
+                ("page_stride", ctypes.c_int64), ("num_pages", ctypes.c_int64),
+                ("layer_ptrs", ctypes.POINTER(ctypes.c_void_p))]
 
 
 class KvError(RuntimeError):
@@ -91,6 +99,10 @@ def _open():
         "kv_check": ([ctypes.POINTER(KvCache), ctypes.POINTER(KvLayout), i64, i64, P, ctypes.c_int], i32),
         "kv_store": ([ctypes.POINTER(KvCache), P, i64, P, P, P], i32),
         "kv_load": ([ctypes.POINTER(KvCache), P, i64, P, P, P], i32),
+        "kv_pool_state_slot": ([P, i64], P),
+        "kv_check_state": ([ctypes.POINTER(KvState), i64, i64, i64, P, P, ctypes.c_int], i32),
+        "kv_store_state": ([ctypes.POINTER(KvState), P, i64, P, P, P], i32),
+        "kv_load_state": ([ctypes.POINTER(KvState), P, i64, P, P, P], i32),
         "kv_last_error": ([], ctypes.c_char_p),
         "kv_status_name": ([i32], ctypes.c_char_p),
         "kv_version": ([], ctypes.c_char_p),
@@ -106,7 +118,8 @@ _lib = _open()
 
 EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slot", "kv_pool_slot_bytes",
            "kv_pool_num_slots", "kv_pool_set_mode", "kv_pool_async_error", "kv_pool_kernel_stats", "kv_check",
-           "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version")
+           "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version", "kv_pool_state_slot",
+           "kv_check_state", "kv_store_state", "kv_load_state")
 
 
 def kv_last_error() -> str:
@@ -188,10 +201,11 @@ def _stream_handle(stream) -> ctypes.c_void_p:
 
 
 def kv_pool_create(layout: KvLayout, num_slots: int, mode="staged", host_kind=KV_HOST_COHERENT,
-                   staging_slots=0, chunks_per_batch=0, side_streams=0, profile=False) -> Pool:
+                   staging_slots=0, chunks_per_batch=0, side_streams=0, profile=False, num_state_slots=0,
+                   state_slot_bytes=0) -> Pool:
     m = MODES[mode] if isinstance(mode, str) else int(mode)
     opts = KvPoolOptions(m, int(host_kind), int(staging_slots), int(chunks_per_batch), int(side_streams),
-                         1 if profile else 0)
+                         1 if profile else 0, int(num_state_slots), int(state_slot_bytes))
     out = ctypes.c_void_p()
     _raise(_lib.kv_pool_create(ctypes.byref(layout), int(num_slots), ctypes.byref(opts), ctypes.byref(out)))
     return Pool(out, layout)
@@ -229,9 +243,11 @@ def kv_pool_async_error(pool: Pool, clear: bool = False) -> int:
 
 
 def kv_pool_kernel_stats(pool: Pool, which: str, reset: bool = False):
-    """(launches, total_ms, algorithmic_bytes) of the pack or unpack kernels since the last reset."""
+    """(launches, total_ms, algorithmic_bytes) of the pack, unpack, state_pack or state_unpack
+    kernels since the last reset."""
     n, ms, b = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double()
-    _raise(_lib.kv_pool_kernel_stats(pool.handle, {"pack": 0, "unpack": 1}[which], 1 if reset else 0,
+    kinds = {"pack": 0, "unpack": 1, "state_pack": 2, "state_unpack": 3}
+    _raise(_lib.kv_pool_kernel_stats(pool.handle, kinds[which], 1 if reset else 0,
                                      ctypes.byref(n), ctypes.byref(ms), ctypes.byref(b)))
     return int(n.value), float(ms.value), float(b.value)
 
@@ -241,6 +257,80 @@ def pool_view(pool: Pool) -> np.ndarray:
     info = kv_pool_get_info(pool)
     buf = (ctypes.c_uint8 * info["pool_bytes"]).from_address(info["host_base"])
     return np.ctypeslib.as_array(buf)
+
+
+def state_view(pool: Pool) -> np.ndarray:
+    """The pool's state area as a host uint8 numpy array (empty without one)."""
+    info = kv_pool_get_info(pool)
+    nbytes = info["num_state_slots"] * info["state_slot_bytes"]
+    if not nbytes:
+        return np.zeros(0, dtype=np.uint8)
+    buf = (ctypes.c_uint8 * nbytes).from_address(info["state_host_base"])
+    return np.ctypeslib.as_array(buf)
+
+
+def kv_pool_state_slot(pool: Pool, slot: int) -> int:
+    return _lib.kv_pool_state_slot(pool.handle, int(slot)) or 0
+
+
+class State:
+    """A replica's recurrent-state page buffers as the C ABI sees them.
+
+    ``layers``: one tensor [G][num_pages][...] or a list of G per-layer tensors whose bytes
+    hold num_pages pages ``page_stride_bytes`` apart (0 = page_bytes).
+    """
+
+    def __init__(self, layers, page_bytes: int, num_pages: int, page_stride_bytes: int = 0):
+        if isinstance(layers, torch.Tensor):
+            tensors = [layers[g] for g in range(layers.shape[0])]
+            self._keep = [layers]
+        else:
+            tensors = list(layers)
+            self._keep = tensors
+        if not tensors:
+            raise ValueError("at least one recurrent layer buffer is needed")
+        dev = tensors[0].device
+        if dev.type != "cuda":
+            raise ValueError("state layers must be device tensors")
+        stride = int(page_stride_bytes or page_bytes)
+        need = (int(num_pages) - 1) * stride + int(page_bytes)
+        for g, t in enumerate(tensors):
+            if t.device != dev or not t.is_contiguous() or t.numel() * t.element_size() < need:
+                raise ValueError(f"state layer {g}: need a contiguous device buffer of >= {need} bytes on {dev}")
+        self._ptrs = (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+        self.struct = KvState(len(tensors), int(dev.index if dev.index is not None else 0), int(page_bytes),
+                              int(page_stride_bytes), int(num_pages),
+                              ctypes.cast(self._ptrs, ctypes.POINTER(ctypes.c_void_p)))
+
+
+def kv_check_state(state, pool_state_slot_bytes: int, pool_state_slots: int, n: int, pages, slot_ids,
+                   for_store: bool) -> int:
+    """``state``: a State or a KvState structure."""
+    struct = state.struct if isinstance(state, State) else state
+    pg, pp = _chunk_ids(pages) if pages is not None else (None, None)
+    si, sp = _chunk_ids(slot_ids) if slot_ids is not None else (None, None)
+    return int(_lib.kv_check_state(ctypes.byref(struct), int(pool_state_slot_bytes), int(pool_state_slots), int(n),
+                                   pp, sp, 1 if for_store else 0))
+
+
+def _state_args(pages, slot_ids):
+    pg, pp = _chunk_ids(pages)
+    si, sp = _chunk_ids(slot_ids)
+    if pg.size != si.size:
+        raise ValueError(f"{pg.size} pages but {si.size} slot ids")
+    return pg, pp, si, sp
+
+
+def kv_store_state(state: State, pages, pool: Pool, slot_ids, stream=None) -> None:
+    pg, pp, si, sp = _state_args(pages, slot_ids)
+    _raise(_lib.kv_store_state(ctypes.byref(state.struct), pp, int(pg.size), pool.handle, sp,
+                               _stream_handle(stream)))
+
+
+def kv_load_state(state: State, pages, pool: Pool, slot_ids, stream=None) -> None:
+    pg, pp, si, sp = _state_args(pages, slot_ids)
+    _raise(_lib.kv_load_state(ctypes.byref(state.struct), pp, int(pg.size), pool.handle, sp,
+                              _stream_handle(stream)))
 
 
 def _chunk_ids(chunk_ids):

@@ -23,7 +23,7 @@ def test_header_declares_expected_surface():
     names = _declared()
     for must in ("kv_store", "kv_load", "kv_pool_create", "kv_pool_destroy", "kv_last_error", "kv_check"):
         assert must in names
-    assert len(names) == 15
+    assert len(names) == 19
 
 
 def test_library_exports_every_declared_symbol():
@@ -122,3 +122,58 @@ def test_kv_check_agrees_with_oracle_validation():
         assert (got == kvx.KV_OK) == (want == oracle.OK), (L, H, D, E, BS, C, n, slots, ids, store, got)
         agree += 1
     assert agree > 100
+
+
+def _fake_state(kvx, G, page_bytes, num_pages, stride=0, align=16, ptr_base=0x7E0000000000):
+    ptrs = (ctypes.c_void_p * G)(*[ptr_base + g * (1 << 32) + (align % 16) for g in range(G)])
+    st = kvx.KvState(G, 0, page_bytes, stride, num_pages, ctypes.cast(ptrs, ctypes.POINTER(ctypes.c_void_p)))
+    st._keep = ptrs
+    return st
+
+
+def test_kv_check_state_rules():
+    from paper_2609_15021_amd import kvx
+    st = _fake_state(kvx, 3, 4096, 8)
+    S = 3 * 4096
+    assert kvx.kv_check_state(st, S, 4, 2, [0, 7], [3, 0], True) == kvx.KV_OK, kvx.kv_last_error()
+    assert kvx.kv_check_state(st, S, 4, 0, None, None, True) == kvx.KV_OK
+    assert kvx.kv_check_state(st, S + 16, 4, 1, [0], [0], True) == kvx.KV_EINVAL     # snapshot format differs
+    assert "differs" in kvx.kv_last_error()
+    assert kvx.kv_check_state(st, S, 4, 1, [8], [0], True) == kvx.KV_EINVAL          # page out of range
+    assert kvx.kv_check_state(st, S, 4, 1, [0], [4], True) == kvx.KV_EINVAL          # slot out of range
+    assert kvx.kv_check_state(st, S, 4, 2, [0, 1], [2, 2], True) == kvx.KV_EINVAL    # store writes a slot twice
+    assert kvx.kv_check_state(st, S, 4, 2, [0, 1], [2, 2], False) == kvx.KV_OK       # a load reads it twice
+    assert kvx.kv_check_state(st, S, 4, 2, [5, 5], [0, 1], False) == kvx.KV_EINVAL   # load writes a page twice
+    assert kvx.kv_check_state(st, S, 4, 2, [5, 5], [0, 1], True) == kvx.KV_OK
+    assert kvx.kv_check_state(st, S, 4, -1, [0], [0], True) == kvx.KV_EINVAL
+    assert kvx.kv_check_state(st, S, 4, 1, None, [0], True) == kvx.KV_EINVAL
+    assert kvx.kv_check_state(_fake_state(kvx, 3, 4096, 8, stride=2048), S, 4, 1, [0], [0], True) == kvx.KV_EINVAL
+    assert kvx.kv_check_state(_fake_state(kvx, 3, 4096, 8, stride=4104), S, 4, 1, [0], [0], True) == \
+        kvx.KV_EUNSUPPORTED
+    assert kvx.kv_check_state(_fake_state(kvx, 3, 4096, 8, align=8), S, 4, 1, [0], [0], True) == \
+        kvx.KV_EUNSUPPORTED
+    assert kvx.kv_check_state(_fake_state(kvx, 3, 40, 8), 120, 4, 1, [0], [0], True) == kvx.KV_EUNSUPPORTED
+    assert kvx.kv_check_state(_fake_state(kvx, 65, 16, 8), 65 * 16, 4, 1, [0], [0], True) == kvx.KV_EUNSUPPORTED
+    assert kvx.kv_check_state(_fake_state(kvx, 0, 16, 8), 0, 4, 1, [0], [0], True) == kvx.KV_EINVAL
+    assert kvx.kv_check_state(_fake_state(kvx, 3, 4096, 0), S, 4, 1, [0], [0], True) == kvx.KV_EINVAL
+
+
+def test_kv_check_state_agrees_with_oracle_validation():
+    from paper_2609_15021_amd import kvx
+    rng = np.random.default_rng(99)
+    checked = 0
+    for _ in range(400):
+        G = int(rng.integers(1, 5))
+        pb = int(rng.choice([16, 48, 4096]))
+        stride = int(rng.choice([0, pb, pb + 16, pb // 2 // 16 * 16 or 16]))
+        npages = int(rng.integers(1, 6))
+        n = int(rng.integers(-1, 5))
+        slots = int(rng.integers(0, 5))
+        pages = rng.integers(-1, npages + 1, size=max(n, 0))
+        ids = rng.integers(-1, slots + 1, size=max(n, 0))
+        store = bool(rng.integers(0, 2))
+        got = kvx.kv_check_state(_fake_state(kvx, G, pb, npages, stride), G * pb, slots, n, pages, ids, store)
+        want = oracle.state_validate(G, pb, stride or pb, npages, pages, n, slots, ids, store)
+        assert (got == kvx.KV_OK) == (want == oracle.OK), (G, pb, stride, npages, n, slots, pages, ids, store)
+        checked += 1
+    assert checked == 400

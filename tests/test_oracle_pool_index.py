@@ -1,0 +1,151 @@
+"""Pins for the pool-index reference model (CPU only): textbook LRU behaviour, the paper's
+whole-chunk hit counts and salt control, aligned recovery, two-phase stores and invariants."""
+import numpy as np
+
+from oracle.pool_index import ENOMEM, PoolIndexModel
+from oracle.recovery import KV, STATE, restorable_chunks
+
+
+def _store(m, salt, toks, n=None):
+    n = len(toks) if n is None else n
+    st, slots, new = m.reserve(salt, toks, n)
+    assert st == 0
+    assert m.commit(slots, new, True) == 0
+    return slots
+
+
+def test_textbook_lru_eviction():
+    """Capacity 3, one chunk per prompt: store A, B, C; use A; store D -> B (least recently used) goes."""
+    m = PoolIndexModel(chunk_tokens=4, num_slots=3)
+    A, B, C, D = ([k] * 4 for k in range(1, 5))
+    for p in (A, B, C):
+        _store(m, 0, p)
+    assert m.lookup(0, A, 4)[1] == 1
+    _store(m, 0, D)
+    assert [m.lookup(0, p, 4)[1] for p in (A, B, C, D)] == [1, 0, 1, 1]
+    assert m.stats()["evictions"] == 1
+
+
+def test_paper_whole_chunk_hits_and_salt():
+    """Sec. 3.1-3.2: hits are whole 1,568-token chunks (25,088 = 16 chunks, 127,008 = 81), and a
+    new cache salt forces zero hits on identical tokens."""
+    C = 1568
+    m = PoolIndexModel(C, num_slots=200)
+    rng = np.random.default_rng(5)
+    prompt = rng.integers(0, 150000, size=127008 + 700).tolist()
+    _store(m, 11, prompt)
+    kv, hit, slots, _ = m.lookup(11, prompt, len(prompt))
+    assert hit * C == 127008 and kv == 81 and len(set(slots)) == 81
+    assert m.lookup(11, prompt, 25088 + 1000)[1] * C == 25088
+    assert m.lookup(12, prompt, len(prompt))[1] == 0
+
+
+def test_prefix_property():
+    m = PoolIndexModel(8, 64)
+    rng = np.random.default_rng(1)
+    a = rng.integers(0, 1000, size=8 * 12).tolist()
+    b = list(a)
+    b[8 * 10 + 3] += 1  # differs inside chunk 10
+    _store(m, 0, a)
+    assert m.lookup(0, b, len(b))[1] == 10
+    b2 = list(a)
+    b2[0] += 1
+    assert m.lookup(0, b2, len(b2))[1] == 0
+
+
+def test_aligned_recovery_follows_the_rule():
+    m = PoolIndexModel(4, 16, num_state_slots=4)
+    toks = list(range(24))
+    slots = m.reserve(0, toks, 24)[1]
+    for i in (1, 3):
+        st, ss, new = m.reserve_state(slots[i])
+        assert st == 0 and new == 1
+        assert m.commit_state(slots[i]) == 0
+    m.commit(slots, [1] * 6, True)
+    flags = [KV | (STATE if i in (1, 3) else 0) for i in range(6)]
+    kv, hit, got, ss = m.lookup(0, toks, 24, require_state=True)
+    assert (kv, hit) == (6, restorable_chunks(flags, True)) == (6, 4)
+    assert ss == m.slot[slots[3]]["state"]
+    assert m.lookup(0, toks, 24)[1] == 6
+
+
+def test_two_phase_store():
+    m = PoolIndexModel(4, 8)
+    toks = list(range(8))
+    st, slots, new = m.reserve(0, toks, 8)
+    assert st == 0 and new == [1, 1]
+    assert m.lookup(0, toks, 8)[1] == 0                    # pending: invisible
+    st2, slots2, new2 = m.reserve(0, toks, 8)              # a second replica reserves the same prefix
+    assert slots2 == slots and new2 == [0, 0]
+    assert m.commit(slots2, new2, True) == 0               # a non-creator's commit publishes nothing
+    assert m.lookup(0, toks, 8)[1] == 0
+    assert m.commit(slots, new, False) == 0                # the creator aborts
+    assert m.lookup(0, toks, 8)[1] == 0 and m.stats()["free_slots"] == 8
+    _store(m, 0, toks)
+    assert m.lookup(0, toks, 8)[1] == 2
+
+
+def test_eviction_trims_prefix_tails_first():
+    m = PoolIndexModel(2, 4)
+    a = list(range(8))                 # 4 chunks
+    _store(m, 0, a)
+    _store(m, 0, [100, 101, 102, 103])  # 2 chunks: evicts a's chunks 3 and 2
+    assert m.lookup(0, a, 8)[1] == 2
+    assert m.stats()["evictions"] == 2
+
+
+def test_pinned_entries_are_never_evicted():
+    m = PoolIndexModel(2, 3)
+    a = list(range(6))
+    _store(m, 0, a)
+    kv, hit, slots, _ = m.lookup(0, a, 6, pin=True)
+    assert hit == 3
+    st, s2, n2 = m.reserve(0, [9, 9, 9, 9], 4)
+    assert st == ENOMEM and m.stats()["free_slots"] == 0 and m.stats()["pending"] == 0
+    assert m.unpin(slots) == 0
+    st, s2, n2 = m.reserve(0, [9, 9, 9, 9], 4)
+    assert st == 0 and n2 == [1, 1]
+
+
+def _invariants(m):
+    for key, s in m.by_key.items():
+        assert m.slot[s]["key"] == key and not m.slot[s]["aborted"]
+    assert set(m.lru) == {s for s, e in m.slot.items() if not e["pending"]}
+    for ss, owner in m.state_owner.items():
+        assert m.slot[owner]["state"] == ss
+    assert set(m.state_lru) <= set(m.state_owner)
+    for s, e in m.slot.items():
+        assert 0 <= s < m.num_slots and e["pins"] >= 0
+        if e["state"] is not None:
+            assert m.state_owner[e["state"]] == s
+            assert (e["state"] in m.state_lru) == (not e["state_pending"])
+
+
+def test_random_sequences_keep_invariants():
+    rng = np.random.default_rng(3)
+    m = PoolIndexModel(4, 12, num_state_slots=3)
+    prompts = [rng.integers(0, 3, size=int(rng.integers(4, 24))).tolist() for _ in range(10)]
+    held = []
+    for _ in range(3000):
+        op = rng.integers(0, 5)
+        p = prompts[rng.integers(0, len(prompts))]
+        if op == 0:
+            st, slots, new = m.reserve(0, p, len(p))
+            if st == 0:
+                if slots and rng.integers(0, 2):
+                    r, ss, nw = m.reserve_state(slots[-1])
+                    if r == 0 and nw:
+                        m.commit_state(slots[-1], bool(rng.integers(0, 4)))
+                held.append((slots, new, bool(rng.integers(0, 5))))
+        elif op == 1 and held:
+            slots, new, ok = held.pop(int(rng.integers(0, len(held))))
+            assert m.commit(slots, new, ok) == 0
+        elif op == 2:
+            kv, hit, slots, ss = m.lookup(0, p, len(p), require_state=bool(rng.integers(0, 2)), pin=True)
+            assert hit <= kv and (ss == -1 or ss in m.state_owner)
+            assert m.unpin(slots) == 0
+        _invariants(m)
+    for slots, new, ok in held:
+        assert m.commit(slots, new, ok) == 0
+    _invariants(m)
+    assert all(e["pins"] == 0 for e in m.slot.values())

@@ -85,6 +85,7 @@ typedef int32_t kv_status;
 #define KV_EHIP (-3)          /* a HIP runtime call failed (name and message in kv_last_error) */
 #define KV_EUNSUPPORTED (-4)  /* valid per the definition, but outside what the GPU path handles */
 #define KV_EASYNC (-5)        /* a device-side check failed in an earlier call (kv_pool_async_error) */
+#define KV_EBUSY (-6)         /* pool index: no slot can be freed (every slot is pinned or pending) */
 
 /* Host transfer modes (chosen explicitly; nothing is selected silently, cf. Sec. 3.2). */
 #define KV_MODE_ZERO_COPY 1u  /* gather/scatter kernels on `stream` access mapped pinned memory directly */
@@ -297,6 +298,102 @@ KV_API kv_status kv_store_state(const kv_state *state, const int64_t *pages, int
  * layer.  Writes only those pages' first page_bytes bytes.  As kv_store_state otherwise. */
 KV_API kv_status kv_load_state(const kv_state *state, const int64_t *pages, int64_t n, kv_pool *pool,
                                const int64_t *slot_ids, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Pool index (host only; no HIP call).  Manages the pool's slots above the
+ * transfer path, as the shared tier of the paper does (Table 1: a fixed RAM
+ * budget of chunks with LRU eviction):
+ *  - a whole chunk i of a prompt is keyed by a 128-bit hash chained over the
+ *    cache salt and tokens [0, (i+1)*C): a key names the whole prefix it
+ *    completes, and a new salt gives new keys (Sec. 3.2: a new cache salt forced
+ *    zero hits).  Only whole chunks are keyed, so hits are whole chunks (Sec.
+ *    3.1-3.2: 25,088 and 127,008 hit tokens are 16 and 81 chunks of 1,568);
+ *  - under aligned recovery (Sec. 2.2) a hit also needs the recurrent snapshot
+ *    at its boundary: the longest run of leading chunks whose last chunk carries
+ *    a committed snapshot;
+ *  - stores are two-phase: kv_index_reserve returns a slot for every whole
+ *    chunk and marks the ones the caller must store (pending entries are
+ *    invisible to lookups and never evicted); after the host has seen the
+ *    stores complete on their stream (Sec. 3.2's host-side completion), the
+ *    caller commits -- or aborts -- them.  Only the caller that created a
+ *    pending entry publishes or aborts it; an aborted entry loses its key at
+ *    once and frees its slot when its last pin is released;
+ *  - a new entry takes the lowest-numbered free slot; with none free, the least
+ *    recently used committed, unpinned entry is evicted (with its snapshot).  An
+ *    operation on a prefix touches its chunks from last to first, so eviction
+ *    trims prefixes from the end.  Snapshots have their own slot budget and LRU;
+ *    evicting one keeps its chunk; a snapshot is evictable only while its chunk
+ *    entry is committed and unpinned.
+ * Pins (reserve, or lookup with KV_LOOKUP_PIN) keep entries from eviction while
+ * their slots are read or written; release them with kv_index_commit or
+ * kv_index_unpin.  All calls on one index are serialised internally.  Slot
+ * numbers are the pool's chunk slots [0, num_slots) and state slots
+ * [0, num_state_slots).
+ * --------------------------------------------------------------------------- */
+typedef struct kv_index kv_index;
+
+#define KV_LOOKUP_REQUIRE_STATE 1u  /* aligned recovery: a hit needs the snapshot at its boundary */
+#define KV_LOOKUP_PIN 2u            /* pin the hit entries (release with kv_index_unpin) */
+
+typedef struct kv_lookup {
+    int64_t kv_chunks;   /* leading whole chunks whose K/V pages are committed */
+    int64_t hit_chunks;  /* restorable chunks (kv_chunks unless KV_LOOKUP_REQUIRE_STATE) */
+    int64_t hit_tokens;  /* hit_chunks * C */
+    int64_t state_slot;  /* state slot of the snapshot after the last hit chunk, or -1 */
+} kv_lookup;
+
+typedef struct kv_index_stats {
+    int64_t entries;          /* committed chunk entries */
+    int64_t pending;          /* reserved, not yet committed or aborted */
+    int64_t free_slots;
+    int64_t state_entries;    /* committed snapshots */
+    int64_t free_state_slots;
+    int64_t evictions;        /* chunk entries evicted */
+    int64_t state_evictions;  /* snapshots evicted */
+} kv_index_stats;
+
+/* An index over num_slots chunk slots of chunk_tokens tokens and num_state_slots
+ * (>= 0) snapshot slots.  KV_EINVAL on chunk_tokens < 1 or num_slots < 1. */
+KV_API kv_status kv_index_create(int32_t chunk_tokens, int64_t num_slots, int64_t num_state_slots,
+                                 kv_index **out);
+KV_API kv_status kv_index_destroy(kv_index *index);  /* NULL is a no-op */
+
+/* The keys of the floor(n_tokens / C) whole chunks of a prompt: keys[2*i], keys[2*i+1]
+ * for chunk i.  tokens: HOST int32[n_tokens]. */
+KV_API kv_status kv_index_keys(const kv_index *index, uint64_t salt, const int32_t *tokens, int64_t n_tokens,
+                               uint64_t *keys);
+
+/* Longest hit of a prompt (see above): slots[0 .. hit_chunks) receive the chunk slots
+ * (slots: HOST int64, room for floor(n_tokens / C)); *out the counts.  Hit entries (and
+ * the snapshot) become the most recently used.  flags: KV_LOOKUP_*. */
+KV_API kv_status kv_index_lookup(kv_index *index, uint64_t salt, const int32_t *tokens, int64_t n_tokens,
+                                 uint32_t flags, int64_t *slots, kv_lookup *out);
+
+/* Release one pin of each listed slot (KV_EINVAL, nothing released, if one is not pinned). */
+KV_API kv_status kv_index_unpin(kv_index *index, const int64_t *slots, int64_t n);
+
+/* Reserve the whole chunks of a prompt: slots[i] and is_new[i] for every chunk
+ * i < *n_chunks = floor(n_tokens / C) (HOST arrays with that much room).  is_new[i] = 1:
+ * a new pending entry the caller stores; 0: an existing (committed or pending) entry.
+ * Every returned entry is pinned.  KV_EBUSY if a slot cannot be freed: the call then
+ * holds nothing (entries it evicted stay evicted). */
+KV_API kv_status kv_index_reserve(kv_index *index, uint64_t salt, const int32_t *tokens, int64_t n_tokens,
+                                  int64_t *slots, uint8_t *is_new, int64_t *n_chunks);
+
+/* Finish a reservation: with ok != 0 the entries this caller created (is_new[i] = 1)
+ * become visible, otherwise they are aborted; every listed pin is released.  Pass
+ * exactly what kv_index_reserve returned.  KV_EINVAL (nothing changed) on a mismatch. */
+KV_API kv_status kv_index_commit(kv_index *index, const int64_t *slots, const uint8_t *is_new, int64_t n,
+                                 int ok);
+
+/* Reserve the snapshot slot for the boundary after the chunk in `slot` (an entry the
+ * caller holds pinned).  *is_new = 1: a new pending snapshot the caller stores (then
+ * kv_index_commit_state); 0: one exists already.  KV_EBUSY if no snapshot slot can be
+ * freed. */
+KV_API kv_status kv_index_reserve_state(kv_index *index, int64_t slot, int64_t *state_slot, int32_t *is_new);
+KV_API kv_status kv_index_commit_state(kv_index *index, int64_t slot, int ok);
+
+KV_API kv_status kv_index_get_stats(kv_index *index, kv_index_stats *out);
 
 /* Thread-local text of the last failure on this thread (HIP error name, message, call site). */
 KV_API const char *kv_last_error(void);

@@ -26,11 +26,11 @@ Rules where the paper is silent (one reading, stated so the library can be held 
 """
 from __future__ import annotations
 
-from collections import OrderedDict
+from collections import Counter, OrderedDict
 
 from oracle.recovery import KV, STATE, restorable_chunks
 
-ENOMEM = -2
+EBUSY = -6
 EINVAL = -1
 
 
@@ -129,8 +129,8 @@ class PoolIndexModel:
         return len(slots), hit, slots[:hit], state_slot
 
     def unpin(self, slots):
-        for s in slots:
-            if s not in self.slot or self.slot[s]["pins"] == 0:
+        for s, times in Counter(slots).items():
+            if s not in self.slot or self.slot[s]["pins"] < times:
                 return EINVAL
         for s in slots:
             self._release(s)
@@ -159,7 +159,7 @@ class PoolIndexModel:
                         self._drop(t)
                     else:
                         self._release(t)
-                return ENOMEM, [], []
+                return EBUSY, [], []
             self.slot[s] = dict(key=key, pending=True, aborted=False, pins=1, state=None, state_pending=False)
             self.by_key[key] = s
             slots.append(s)
@@ -169,7 +169,7 @@ class PoolIndexModel:
     def commit(self, slots, new, ok=True):
         """Publish (ok) or abort the entries this caller created (new[i] = 1, as reserve returned),
         and release the pins of all of them."""
-        if len(slots) != len(new):
+        if len(slots) != len(new) or len(set(slots)) != len(slots):
             return EINVAL
         for s, is_new in zip(slots, new):
             if s not in self.slot or self.slot[s]["pins"] == 0 or (is_new and not self.slot[s]["pending"]):
@@ -199,7 +199,7 @@ class PoolIndexModel:
             return 0, e["state"], 0
         ss = self._alloc_state()
         if ss is None:
-            return ENOMEM, -1, 0
+            return EBUSY, -1, 0
         e["state"], e["state_pending"] = ss, True
         self.state_owner[ss] = s
         return 0, ss, 1

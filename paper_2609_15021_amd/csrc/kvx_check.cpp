@@ -218,6 +218,8 @@ const char *kv_status_name(kv_status status) {
         return "KV_EUNSUPPORTED";
     case KV_EASYNC:
         return "KV_EASYNC";
+    case KV_EBUSY:
+        return "KV_EBUSY";
     default:
         return "KV_UNKNOWN";
     }

@@ -25,6 +25,7 @@ KV_ENOMEM = -2
 KV_EHIP = -3
 KV_EUNSUPPORTED = -4
 KV_EASYNC = -5
+KV_EBUSY = -6
 
 KV_MODE_ZERO_COPY = 1
 KV_MODE_STAGED = 2
@@ -33,6 +34,8 @@ KV_HOST_NONCOHERENT = 1
 KV_ASYNC_BAD_BLOCK = 1
 KV_BLOCK_HND = 0
 KV_BLOCK_NHD = 1
+KV_LOOKUP_REQUIRE_STATE = 1
+KV_LOOKUP_PIN = 2
 
 MODES = {"zero_copy": KV_MODE_ZERO_COPY, "staged": KV_MODE_STAGED}
 
@@ -74,6 +77,16 @@ class KvState(ctypes.Structure):
                 ("layer_ptrs", ctypes.POINTER(ctypes.c_void_p))]
 
 
+class KvLookup(ctypes.Structure):
+    _fields_ = [("kv_chunks", ctypes.c_int64), ("hit_chunks", ctypes.c_int64), ("hit_tokens", ctypes.c_int64),
+                ("state_slot", ctypes.c_int64)]
+
+
+class KvIndexStats(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int64) for name in ("entries", "pending", "free_slots", "state_entries",
+                                                      "free_state_slots", "evictions", "state_evictions")]
+
+
 class KvError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(message)
@@ -103,6 +116,16 @@ def _open():
         "kv_check_state": ([ctypes.POINTER(KvState), i64, i64, i64, P, P, ctypes.c_int], i32),
         "kv_store_state": ([ctypes.POINTER(KvState), P, i64, P, P, P], i32),
         "kv_load_state": ([ctypes.POINTER(KvState), P, i64, P, P, P], i32),
+        "kv_index_create": ([i32, i64, i64, ctypes.POINTER(P)], i32),
+        "kv_index_destroy": ([P], i32),
+        "kv_index_keys": ([P, ctypes.c_uint64, P, i64, P], i32),
+        "kv_index_lookup": ([P, ctypes.c_uint64, P, i64, u32, P, ctypes.POINTER(KvLookup)], i32),
+        "kv_index_unpin": ([P, P, i64], i32),
+        "kv_index_reserve": ([P, ctypes.c_uint64, P, i64, P, P, ctypes.POINTER(i64)], i32),
+        "kv_index_commit": ([P, P, P, i64, ctypes.c_int], i32),
+        "kv_index_reserve_state": ([P, i64, ctypes.POINTER(i64), ctypes.POINTER(i32)], i32),
+        "kv_index_commit_state": ([P, i64, ctypes.c_int], i32),
+        "kv_index_get_stats": ([P, ctypes.POINTER(KvIndexStats)], i32),
         "kv_last_error": ([], ctypes.c_char_p),
         "kv_status_name": ([i32], ctypes.c_char_p),
         "kv_version": ([], ctypes.c_char_p),
@@ -119,7 +142,9 @@ _lib = _open()
 EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slot", "kv_pool_slot_bytes",
            "kv_pool_num_slots", "kv_pool_set_mode", "kv_pool_async_error", "kv_pool_kernel_stats", "kv_check",
            "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version", "kv_pool_state_slot",
-           "kv_check_state", "kv_store_state", "kv_load_state")
+           "kv_check_state", "kv_store_state", "kv_load_state", "kv_index_create", "kv_index_destroy",
+           "kv_index_keys", "kv_index_lookup", "kv_index_unpin", "kv_index_reserve", "kv_index_commit",
+           "kv_index_reserve_state", "kv_index_commit_state", "kv_index_get_stats")
 
 
 def kv_last_error() -> str:
@@ -363,3 +388,106 @@ def kv_load(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, str
     ids, ptr = _chunk_ids(chunk_ids)
     _raise(_lib.kv_load(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
                         pool.handle, ptr, _stream_handle(stream)))
+
+
+# ---- Pool index (host only) --------------------------------------------------------------
+
+class Index:
+    """Owning handle of a kv_index."""
+
+    def __init__(self, handle: ctypes.c_void_p, chunk_tokens: int):
+        self.handle = handle
+        self.chunk_tokens = chunk_tokens
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            try:
+                _lib.kv_index_destroy(self.handle)
+            except Exception:
+                pass
+            self.handle = None
+
+
+def _tokens(tokens):
+    t = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+    return t, (ctypes.c_void_p(t.ctypes.data) if t.size else None)
+
+
+def _i64_array(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.int64))
+    return a, (ctypes.c_void_p(a.ctypes.data) if a.size else None)
+
+
+def kv_index_create(chunk_tokens: int, num_slots: int, num_state_slots: int = 0) -> Index:
+    out = ctypes.c_void_p()
+    _raise(_lib.kv_index_create(int(chunk_tokens), int(num_slots), int(num_state_slots), ctypes.byref(out)))
+    return Index(out, int(chunk_tokens))
+
+
+def kv_index_destroy(index: Index) -> None:
+    h, index.handle = index.handle, None
+    _raise(_lib.kv_index_destroy(h))
+
+
+def kv_index_keys(index: Index, salt: int, tokens) -> np.ndarray:
+    t, tp = _tokens(tokens)
+    keys = np.zeros((t.size // index.chunk_tokens, 2), dtype=np.uint64)
+    _raise(_lib.kv_index_keys(index.handle, int(salt) & 0xFFFFFFFFFFFFFFFF, tp, int(t.size),
+                              ctypes.c_void_p(keys.ctypes.data) if keys.size else None))
+    return keys
+
+
+def kv_index_lookup(index: Index, salt: int, tokens, require_state=False, pin=False) -> dict:
+    t, tp = _tokens(tokens)
+    slots = np.zeros(t.size // index.chunk_tokens, dtype=np.int64)
+    out = KvLookup()
+    flags = (KV_LOOKUP_REQUIRE_STATE if require_state else 0) | (KV_LOOKUP_PIN if pin else 0)
+    _raise(_lib.kv_index_lookup(index.handle, int(salt) & 0xFFFFFFFFFFFFFFFF, tp, int(t.size), flags,
+                                ctypes.c_void_p(slots.ctypes.data) if slots.size else None, ctypes.byref(out)))
+    r = {name: int(getattr(out, name)) for name, _ in KvLookup._fields_}
+    r["slots"] = slots[:r["hit_chunks"]].copy()
+    return r
+
+
+def kv_index_unpin(index: Index, slots) -> None:
+    a, p = _i64_array(slots)
+    _raise(_lib.kv_index_unpin(index.handle, p, int(a.size)))
+
+
+def kv_index_reserve(index: Index, salt: int, tokens):
+    """(slots int64[nc], is_new uint8[nc]) for the whole chunks of the prompt; KvError(KV_EBUSY) if full."""
+    t, tp = _tokens(tokens)
+    nc = t.size // index.chunk_tokens
+    slots = np.zeros(nc, dtype=np.int64)
+    is_new = np.zeros(nc, dtype=np.uint8)
+    n = ctypes.c_int64()
+    _raise(_lib.kv_index_reserve(index.handle, int(salt) & 0xFFFFFFFFFFFFFFFF, tp, int(t.size),
+                                 ctypes.c_void_p(slots.ctypes.data) if nc else None,
+                                 ctypes.c_void_p(is_new.ctypes.data) if nc else None, ctypes.byref(n)))
+    return slots, is_new
+
+
+def kv_index_commit(index: Index, slots, is_new, ok: bool = True) -> None:
+    a, p = _i64_array(slots)
+    b = np.ascontiguousarray(np.asarray(is_new, dtype=np.uint8))
+    if a.size != b.size:
+        raise ValueError("slots and is_new differ in length")
+    _raise(_lib.kv_index_commit(index.handle, p, ctypes.c_void_p(b.ctypes.data) if b.size else None, int(a.size),
+                                1 if ok else 0))
+
+
+def kv_index_reserve_state(index: Index, slot: int):
+    """(state_slot, is_new) of the snapshot after the chunk in ``slot``."""
+    ss, new = ctypes.c_int64(), ctypes.c_int32()
+    _raise(_lib.kv_index_reserve_state(index.handle, int(slot), ctypes.byref(ss), ctypes.byref(new)))
+    return int(ss.value), int(new.value)
+
+
+def kv_index_commit_state(index: Index, slot: int, ok: bool = True) -> None:
+    _raise(_lib.kv_index_commit_state(index.handle, int(slot), 1 if ok else 0))
+
+
+def kv_index_get_stats(index: Index) -> dict:
+    st = KvIndexStats()
+    _raise(_lib.kv_index_get_stats(index.handle, ctypes.byref(st)))
+    return {name: int(getattr(st, name)) for name, _ in KvIndexStats._fields_}

@@ -2,7 +2,7 @@
 whole-chunk hit counts and salt control, aligned recovery, two-phase stores and invariants."""
 import numpy as np
 
-from oracle.pool_index import ENOMEM, PoolIndexModel
+from oracle.pool_index import EBUSY, PoolIndexModel
 from oracle.recovery import KV, STATE, restorable_chunks
 
 
@@ -101,7 +101,7 @@ def test_pinned_entries_are_never_evicted():
     kv, hit, slots, _ = m.lookup(0, a, 6, pin=True)
     assert hit == 3
     st, s2, n2 = m.reserve(0, [9, 9, 9, 9], 4)
-    assert st == ENOMEM and m.stats()["free_slots"] == 0 and m.stats()["pending"] == 0
+    assert st == EBUSY and m.stats()["free_slots"] == 0 and m.stats()["pending"] == 0
     assert m.unpin(slots) == 0
     st, s2, n2 = m.reserve(0, [9, 9, 9, 9], 4)
     assert st == 0 and n2 == [1, 1]

@@ -15,7 +15,9 @@ dominant pack/unpack kernel (timed live with HIP events on its stream), the
 host-link rate against the measured pinned-copy peak, a zero-copy comparison,
 a sampled round-trip check against the seeded generator, and the CPU oracle's
 own throughput on a bounded sample (the cpu_baseline; the only use of the
-oracle here).
+oracle here).  Side legs: the paper-native attention layout, recurrent-state
+snapshot pages of a hybrid model, and the host-side pool index at the paper's
+256 GiB tier size.
 """
 from __future__ import annotations
 
@@ -56,6 +58,10 @@ def parse():
     ap.add_argument("--no-paper-layout", action="store_true", help="skip the paper-native layout measurement")
     ap.add_argument("--paper-layout-only", action="store_true",
                     help="only measure the paper-native layout and print its JSON object (run by the main bench)")
+    ap.add_argument("--no-state", action="store_true", help="skip the recurrent-state snapshot measurement")
+    ap.add_argument("--state-only", action="store_true",
+                    help="only measure recurrent-state snapshots and print its JSON object (run by the main bench)")
+    ap.add_argument("--no-index", action="store_true", help="skip the pool-index measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (PMC counter scale reference)")
     return ap.parse_args()
@@ -204,6 +210,146 @@ def paper_layout(np, torch, harness, hg, kvx, mode, dev, reps=3):
             "round_trip": "bit-exact (whole prefix, on device)" if ok else "FAILED"}, ok
 
 
+# Recurrent-state page of a GDN layer of a 27B-class hybrid model: 48 value heads of 128x128
+# fp32 recurrent state plus a 3-step convolution state over 10,240 bf16 channels (the paper
+# gives no state sizes; this geometry is an assumption).
+GDN_LAYERS, GDN_PAGE = 48, 3 * 1024 * 1024 + 3 * 10240 * 2
+
+
+def state_snapshots(np, torch, hg, kvx, mode, dev, reps=3, n_snap=16, n_pages=20):
+    """Store 16 boundary snapshots (48 recurrent layers x 3 MiB + 60 KiB pages each, 2.46 GB) into
+    the pool's state area and load them into other pages of a second allocation (Sec. 2.2)."""
+    G, pb = GDN_LAYERS, GDN_PAGE
+    layout = kvx.make_layout(L, H, D, E, BS, C)
+    pool = kvx.kv_pool_create(layout, 1, mode, profile=True, num_state_slots=n_snap, state_slot_bytes=G * pb)
+    a = torch.empty((G, n_pages, pb), dtype=torch.uint8, device=dev)
+    b = torch.zeros_like(a)
+    hg.fill_values(a, 0, 0x5EED, "raw", 1)
+    rng = np.random.default_rng(2609)
+    pages_a = rng.permutation(n_pages)[:n_snap]
+    pages_b = rng.permutation(n_pages)[:n_snap]
+    slots = rng.permutation(n_snap)
+    sa, sb = kvx.State(a, pb, n_pages), kvx.State(b, pb, n_pages)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    kvx.kv_store_state(sa, pages_a, pool, slots, s)
+    kvx.kv_load_state(sb, pages_b, pool, slots, s)
+    s.synchronize()
+    for w in ("state_pack", "state_unpack"):
+        kvx.kv_pool_kernel_stats(pool, w, reset=True)
+    st, ld = [], []
+    for _ in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(s)
+        kvx.kv_store_state(sa, pages_a, pool, slots, s)
+        e[1].record(s)
+        kvx.kv_load_state(sb, pages_b, pool, slots, s)
+        e[2].record(s)
+        s.synchronize()
+        st.append(e[0].elapsed_time(e[1]) / 1e3)
+        ld.append(e[1].elapsed_time(e[2]) / 1e3)
+    N = n_snap * G * pb
+    kern = {}
+    for w in ("state_pack", "state_unpack"):
+        launches, ms, alg = kvx.kv_pool_kernel_stats(pool, w, reset=True)
+        if launches and ms:
+            kern[w] = {"launch_groups": launches, "avg_group_ms": round(ms / launches, 4),
+                       "achieved_GBps": round(alg / (ms / 1e3) / 1e9, 1),
+                       "frac_of_hbm_peak": round(alg / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)}
+    ia = torch.from_numpy(pages_a.astype(np.int64)).to(dev)
+    ib = torch.from_numpy(pages_b.astype(np.int64)).to(dev)
+    ok = bool(torch.equal(a[:, ia], b[:, ib]))
+    untouched = sorted(set(range(n_pages)) - set(pages_b.tolist()))
+    ok = ok and not bool(b[:, untouched].any())
+    kvx.kv_pool_destroy(pool)
+    del a, b
+    torch.cuda.empty_cache()
+    return {"workload": f"{n_snap} boundary snapshots of {G} recurrent layers, {pb:,}-byte opaque pages "
+                        f"({N / 1e9:.2f} GB per direction), store then load into other pages of a second allocation",
+            "bytes_per_direction": N, "mode": mode,
+            "store_GBps": round(N / statistics.median(st) / 1e9, 3),
+            "load_GBps": round(N / statistics.median(ld) / 1e9, 3), "kernels": kern,
+            "round_trip": "bit-exact (all snapshot pages; other pages untouched)" if ok else "FAILED"}, ok
+
+
+# The paper's shared tier (Table 1): 256 GiB of 1,568-token chunks of its attention layout
+# (16 layers x 4 KV heads x 256 x 1 byte x 2 = 32 KiB per token, 49 MiB per chunk).
+TIER_C = 1568
+TIER_SLOTS = (256 << 30) // (TIER_C * 32768)
+
+
+def index_requests(np, n_docs=96, n_requests=2000, doc_tokens=131072, suffix=2000):
+    """A seeded request stream for the pool index: each prompt is one of n_docs 128k-token
+    documents (Zipf-like popularity) plus a fresh suffix."""
+    rng = np.random.default_rng(1568)
+    docs = [rng.integers(0, 151000, size=doc_tokens).astype(np.int32) for _ in range(n_docs)]
+    w = 1.0 / np.arange(1, n_docs + 1)
+    pick = rng.choice(n_docs, size=n_requests, p=w / w.sum())
+    return [np.concatenate([docs[d], rng.integers(0, 151000, size=suffix).astype(np.int32)]) for d in pick]
+
+
+def serve_request(idx_ops, prompt, shared_tokens=131072):
+    """One request against an index: aligned lookup (pinned), release, then reserve the whole
+    prompt, a snapshot at the last chunk boundary inside the shared document, and commit (the
+    stores themselves are GPU work)."""
+    lookup, unpin, reserve, reserve_state, commit_state, commit = idx_ops
+    hit = lookup(prompt)
+    unpin(hit)
+    slots, new = reserve(prompt)
+    k = min(len(slots), shared_tokens // TIER_C)
+    if k:
+        if reserve_state(slots[k - 1]):
+            commit_state(slots[k - 1])
+    commit(slots, new)
+    return hit
+
+
+def pool_index(np, kvx, prompts):
+    x = kvx.kv_index_create(TIER_C, TIER_SLOTS, 512)
+    ops = (lambda p: kvx.kv_index_lookup(x, 1, p, require_state=True, pin=True)["slots"],
+           lambda sl: kvx.kv_index_unpin(x, sl),
+           lambda p: kvx.kv_index_reserve(x, 1, p),
+           lambda s: kvx.kv_index_reserve_state(x, s)[1],
+           lambda s: kvx.kv_index_commit_state(x, s),
+           lambda sl, nw: kvx.kv_index_commit(x, sl, nw))
+    hits = 0
+    t0 = time.perf_counter()
+    for p in prompts:
+        hits += len(serve_request(ops, p))
+    dt = time.perf_counter() - t0
+    st = kvx.kv_index_get_stats(x)
+    kvx.kv_index_destroy(x)
+    return {"workload": f"{len(prompts)} requests of 128k-token documents (96 documents, Zipf-like popularity) plus "
+                        f"a 2,000-token suffix: aligned lookup, reserve of all whole chunks, a snapshot at the "
+                        f"document's last chunk boundary, commit; "
+                        f"{TIER_SLOTS:,} slots of {TIER_C:,} tokens (256 GiB tier) and 512 snapshot slots",
+            "requests_per_s": round(len(prompts) / dt, 1), "us_per_request": round(dt / len(prompts) * 1e6, 1),
+            "tokens_keyed_per_s": round(2 * sum(len(p) for p in prompts) / dt / 1e6, 1),
+            "tokens_keyed_unit": "M tokens/s (lookup + reserve)",
+            "hit_chunks": hits, "hit_rate": round(hits / (len(prompts) * (131072 // TIER_C)), 4),
+            "evictions": st["evictions"], "state_evictions": st["state_evictions"], "entries": st["entries"]}
+
+
+def pool_index_oracle(np, model_cls, prompts):
+    """The oracle's exact-key index model on the first requests of the same stream."""
+    m = model_cls(TIER_C, TIER_SLOTS, 512)
+    ops = (lambda p: m.lookup(1, p.tolist(), len(p), require_state=True, pin=True)[2],
+           lambda sl: m.unpin(sl),
+           lambda p: m.reserve(1, p.tolist(), len(p))[1:],
+           lambda s: m.reserve_state(s)[2],
+           lambda s: m.commit_state(s),
+           lambda sl, nw: m.commit(sl, nw))
+    t0, done = time.perf_counter(), 0
+    for p in prompts:
+        serve_request(ops, p)
+        done += 1
+        if time.perf_counter() - t0 > 15.0:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": round(done / dt, 2), "unit": "requests/s", "cores": 1, "kind": "oracle",
+            "sample": f"the first {done} requests of the pool-index stream, single thread"}
+
+
 def cpu_baseline(np, oracle, n_chunks=64):
     """The oracle timed on host cores: store + load of a bounded sample of the workload."""
     rng = np.random.default_rng(2609)
@@ -258,24 +404,35 @@ def main():
         paper, paper_ok = paper_layout(np, torch, harness, hg, kvx, args.mode, dev)
         print(json.dumps(paper), flush=True)
         sys.exit(0 if paper_ok else 1)
+    if args.state_only:
+        res, res_ok = state_snapshots(np, torch, hg, kvx, args.mode, dev)
+        print(json.dumps(res), flush=True)
+        sys.exit(0 if res_ok else 1)
 
-    # The paper-layout leg runs first, in its own process, on fresh memory: on these machines,
+    # The side legs run first, each in its own process, on fresh memory: on these machines,
     # transfers through pools created after large allocations were freed measured ~10% slower
     # (even from a new process), and a serving pool is created once at startup.
-    paper = None
-    if not args.no_paper_layout:
+    def child_leg(flag):
         import subprocess
-        r = subprocess.run([sys.executable, os.path.abspath(__file__), "--paper-layout-only", "--mode", args.mode],
+        r = subprocess.run([sys.executable, os.path.abspath(__file__), flag, "--mode", args.mode],
                            capture_output=True, text=True, timeout=600)
         lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
-        paper = json.loads(lines[-1]) if lines else {"error": r.stderr[-2000:]}
-        paper_ok = r.returncode == 0
-        if lines:
+        return (json.loads(lines[-1]) if lines else {"error": r.stderr[-2000:]}), r.returncode == 0 and bool(lines)
+
+    paper, paper_ok = None, True
+    if not args.no_paper_layout:
+        paper, paper_ok = child_leg("--paper-layout-only")
+        if "error" not in paper:
             log(f"[bench] paper layout 128k: store {paper['store_GBps']} GB/s, load {paper['load_GBps']} GB/s, "
                 f"restore {paper['restore_s_128k']} s, pack {paper['kernels']['pack']['achieved_GBps']} GB/s, "
                 f"unpack {paper['kernels']['unpack']['achieved_GBps']} GB/s; {paper['round_trip']}")
-    else:
-        paper_ok = True
+    state, state_ok = None, True
+    if not args.no_state:
+        state, state_ok = child_leg("--state-only")
+        if "error" not in state:
+            log(f"[bench] state snapshots: store {state['store_GBps']} GB/s, load {state['load_GBps']} GB/s, "
+                f"kernels {json.dumps(state['kernels'])}; {state['round_trip']}")
+    paper_ok = paper_ok and state_ok
 
     layout = kvx.make_layout(L, H, D, E, BS, C)
     n = args.tokens
@@ -425,10 +582,22 @@ def main():
         del ra, rb, ta, tb
         torch.cuda.empty_cache()
 
+    index = None
+    prompts = None
+    if not args.no_index:
+        prompts = index_requests(np)
+        index = pool_index(np, kvx, prompts)
+        log(f"[bench] pool index: {index['requests_per_s']} requests/s ({index['us_per_request']} us each), "
+            f"{index['tokens_keyed_per_s']} M tokens/s keyed, {index['evictions']} evictions")
+
     cpu = None
     if not args.no_cpu_baseline:
-        import oracle  # the CPU baseline leg is the only part of the benchmark that runs the oracle
+        # The CPU baseline leg is the only part of the benchmark that runs the oracle.
+        import oracle
+        from oracle.pool_index import PoolIndexModel
         cpu = cpu_baseline(np, oracle)
+        if index is not None:
+            cpu["pool_index"] = pool_index_oracle(np, PoolIndexModel, prompts)
     if cpu:
         log(f"[bench] cpu oracle: {cpu['value']} GB/s on {cpu['cores']} threads, {cpu['value_1_thread']} GB/s on 1")
 
@@ -457,6 +626,8 @@ def main():
         "parity": parity_msg if ok else f"FAILED: {parity_msg}",
         "parity_256k": parity_256k,
         "paper_layout": paper,
+        "state_snapshots": state,
+        "pool_index": index,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -395,6 +395,59 @@ KV_API kv_status kv_index_commit_state(kv_index *index, int64_t slot, int ok);
 
 KV_API kv_status kv_index_get_stats(kv_index *index, kv_index_stats *out);
 
+/* ---------------------------------------------------------------------------
+ * Tier: one process owns the pool; replicas in other processes store into it
+ * and load from it (the paper's two replicas sharing one host tier, Sec. 2 and
+ * Fig. 1).  A tier process calls kv_tier_serve on a connected stream socket per
+ * replica.  A replica calls kv_tier_store / kv_tier_load on its end.  They pass
+ * its cache as HIP IPC handles: each layer pointer names an allocation that
+ * the tier opens once per connection and closes when the connection ends.  The
+ * handshake is the host-side completion handling of Sec. 3.2 in both
+ * directions:
+ *  - the replica synchronises `stream` before sending, so every producer write
+ *    to its cache (store) and every earlier use of the destination (load) has
+ *    completed;
+ *  - the tier enqueues kv_store / kv_load on its own stream, synchronises it
+ *    and only then replies, so a stored chunk is committed (visible to any
+ *    later request of any replica) and a loaded cache is complete when the
+ *    call returns.
+ * Requests from all connections to one pool are served one at a time.
+ * Device-side faults of a request (KV_ASYNC_*) are returned to its sender as
+ * KV_EASYNC.
+ * --------------------------------------------------------------------------- */
+
+/* Largest allocation shared through IPC (exclusive): opening larger ones has not
+ * returned on the machines this library was measured on. */
+#define KV_IPC_MAX_ALLOCATION_BYTES ((int64_t)2 << 30)
+
+typedef struct kv_ipc_buffer {
+    uint8_t handle[64];  /* hipIpcMemHandle_t of the allocation that holds the buffer */
+    int64_t offset;      /* byte offset of the buffer inside that allocation */
+    int64_t allocation_bytes;
+} kv_ipc_buffer;
+
+/* Export a device pointer of this process.  KV_EUNSUPPORTED if its allocation is
+ * KV_IPC_MAX_ALLOCATION_BYTES or larger, KV_EHIP if the runtime refuses. */
+KV_API kv_status kv_ipc_export(const void *dev_ptr, kv_ipc_buffer *out);
+
+/* Serve one replica connection: read requests from the connected stream socket
+ * `fd` until the peer closes it, run each on `pool` (current device = the
+ * pool's), reply.  Blocks.  Returns KV_OK on an orderly close, an error if the
+ * connection failed or sent a malformed frame (then the socket is left open
+ * for the caller to close). */
+KV_API kv_status kv_tier_serve(kv_pool *pool, int fd);
+
+/* Replica side.  cache: this process's cache (layer pointers are exported);
+ * block_table: HOST int32[ceil(n_tokens / BS)], read before return; chunk_ids:
+ * HOST int64[nc]; stream: synchronised before the request is sent.  Blocks
+ * until the tier replied; returns the tier's status (its message in
+ * kv_last_error) or a transport error (KV_EHIP for HIP, KV_EINVAL for a
+ * closed or failed connection). */
+KV_API kv_status kv_tier_store(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
+                               const int64_t *chunk_ids, void *stream);
+KV_API kv_status kv_tier_load(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
+                              const int64_t *chunk_ids, void *stream);
+
 /* Thread-local text of the last failure on this thread (HIP error name, message, call site). */
 KV_API const char *kv_last_error(void);
 

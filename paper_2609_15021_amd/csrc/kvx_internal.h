@@ -153,4 +153,5 @@ struct kv_pool {
     double total_bytes[4] = {0.0, 0.0, 0.0, 0.0};
 
     std::mutex mu;
+    std::mutex tier_mu;  // serialises tier requests (one request's faults are its own)
 };

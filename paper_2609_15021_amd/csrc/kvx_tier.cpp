@@ -1,0 +1,347 @@
+// Tier: one process owns the pinned pool; replicas in other processes store and load
+// through it over a stream socket, passing their caches as HIP IPC handles.
+//
+// The paper's replicas share one host tier (Sec. 2, Fig. 1) and its fault is a consumer
+// running before its producer completed (Sec. 3.2).  Here a pinned region cannot be
+// registered in a second process, so the process that pinned the pool also runs every
+// copy into and out of it; replicas hand over device memory instead.  Both ends complete
+// on the host before handing over: the replica synchronises its stream before sending,
+// and the tier synchronises its own stream before replying.
+//
+// Frames are native-layout structs (both ends run on one host): a request header, the
+// layers' IPC buffers, the block table and the chunk ids; a reply header and a message.
+#include <sys/socket.h>
+#include <sys/types.h>
+
+#include <array>
+#include <cerrno>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "kvx_internal.h"
+
+namespace {
+
+constexpr uint32_t kMagic = 0x5458564Bu;  // "KVXT"
+constexpr uint32_t kOpStore = 1, kOpLoad = 2;
+constexpr int32_t kMaxLayers = 4096;
+constexpr int64_t kMaxPayload = int64_t(1) << 30;
+
+struct RequestHeader {
+    uint32_t magic;
+    uint32_t op;
+    kv_layout layout;
+    int32_t num_blocks;
+    int32_t block_order;
+    int32_t num_layers;
+    int32_t pad;
+    int64_t block_stride_bytes;
+    int64_t n_tokens;
+    int64_t n_table;   // int32 block-table entries that follow the layers
+    int64_t n_chunks;  // int64 chunk ids that follow the table
+};
+
+struct ReplyHeader {
+    uint32_t magic;
+    int32_t status;
+    uint32_t msg_len;
+    uint32_t pad;
+};
+
+// Whole-buffer socket I/O.  Returns false on EOF or error (errno kept); *eof set on a clean
+// end before the first byte.
+bool read_full(int fd, void *buf, size_t n, bool *eof = nullptr) {
+    auto *p = static_cast<uint8_t *>(buf);
+    size_t done = 0;
+    if (eof)
+        *eof = false;
+    while (done < n) {
+        const ssize_t r = recv(fd, p + done, n - done, 0);
+        if (r == 0) {
+            if (eof && done == 0)
+                *eof = true;
+            return false;
+        }
+        if (r < 0) {
+            if (errno == EINTR)
+                continue;
+            return false;
+        }
+        done += static_cast<size_t>(r);
+    }
+    return true;
+}
+
+bool write_full(int fd, const void *buf, size_t n) {
+    const auto *p = static_cast<const uint8_t *>(buf);
+    size_t done = 0;
+    while (done < n) {
+        const ssize_t r = send(fd, p + done, n - done, MSG_NOSIGNAL);
+        if (r < 0) {
+            if (errno == EINTR)
+                continue;
+            return false;
+        }
+        done += static_cast<size_t>(r);
+    }
+    return true;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// The tier end of one connection.
+class Connection {
+  public:
+    Connection(kv_pool *pool, int fd) : pool_(pool), fd_(fd) {}
+
+    ~Connection() {
+        if (stream_) {
+            (void)hipStreamSynchronize(stream_);
+            (void)hipStreamDestroy(stream_);
+        }
+        for (auto &kv : opened_)
+            (void)hipIpcCloseMemHandle(kv.second.base);
+        if (table_)
+            (void)hipFree(table_);
+    }
+
+    kv_status serve() {
+        KVX_HIP(hipSetDevice(pool_->device));
+        KVX_HIP(hipStreamCreateWithFlags(&stream_, hipStreamNonBlocking));
+        for (;;) {
+            RequestHeader h;
+            bool eof = false;
+            if (!read_full(fd_, &h, sizeof(h), &eof)) {
+                if (eof)
+                    return KV_OK;
+                return kvx::fail(KV_EINVAL, "tier: connection failed while reading a request (%s)",
+                                 std::strerror(errno));
+            }
+            if (h.magic != kMagic || (h.op != kOpStore && h.op != kOpLoad) || h.num_layers < 1 ||
+                h.num_layers > kMaxLayers || h.n_table < 0 || h.n_chunks < 0)
+                return kvx::fail(KV_EINVAL, "tier: malformed request header");
+            const int64_t payload = static_cast<int64_t>(h.num_layers) * int64_t(sizeof(kv_ipc_buffer)) +
+                                    h.n_table * int64_t(sizeof(int32_t)) + h.n_chunks * int64_t(sizeof(int64_t));
+            if (payload > kMaxPayload)
+                return kvx::fail(KV_EINVAL, "tier: request payload of %lld bytes is too large",
+                                 static_cast<long long>(payload));
+            bufs_.resize(static_cast<size_t>(h.num_layers));
+            table_host_.resize(static_cast<size_t>(h.n_table));
+            ids_.resize(static_cast<size_t>(h.n_chunks));
+            if (!read_full(fd_, bufs_.data(), bufs_.size() * sizeof(kv_ipc_buffer)) ||
+                !read_full(fd_, table_host_.data(), table_host_.size() * sizeof(int32_t)) ||
+                !read_full(fd_, ids_.data(), ids_.size() * sizeof(int64_t)))
+                return kvx::fail(KV_EINVAL, "tier: connection failed while reading a request body");
+
+            kv_status st;
+            {
+                std::lock_guard<std::mutex> lock(pool_->tier_mu);
+                st = execute(h);
+            }
+            const std::string msg = st == KV_OK ? std::string() : std::string(kv_last_error());
+            ReplyHeader r{kMagic, st, static_cast<uint32_t>(msg.size()), 0};
+            if (!write_full(fd_, &r, sizeof(r)) || !write_full(fd_, msg.data(), msg.size()))
+                return kvx::fail(KV_EINVAL, "tier: connection failed while replying (%s)", std::strerror(errno));
+        }
+    }
+
+  private:
+    kv_status execute(const RequestHeader &h) {
+        const kv_layout &lay = h.layout;
+        if (lay.block_size < 1 || lay.chunk_tokens < 1 || h.n_tokens < 0 || lay.num_layers != h.num_layers)
+            return kvx::fail(KV_EINVAL, "tier: request layout or length is invalid");
+        if (h.n_table != ceil_div(h.n_tokens, lay.block_size) || h.n_chunks != ceil_div(h.n_tokens, lay.chunk_tokens))
+            return kvx::fail(KV_EINVAL, "tier: block table or chunk ids do not match n_tokens");
+        if (h.n_tokens == 0)
+            return KV_OK;
+        kv_status vst = kvx::check_layout(lay);
+        if (vst != KV_OK)
+            return vst;
+        if (h.block_stride_bytes < 0)
+            return kvx::fail(KV_EINVAL, "tier: negative block stride");
+        const kvx::Geometry g = kvx::geometry(lay, h.block_stride_bytes);
+
+        // Map the replica's layers (each allocation once per connection).
+        layers_.resize(static_cast<size_t>(h.num_layers));
+        for (int32_t l = 0; l < h.num_layers; ++l) {
+            std::array<uint8_t, 64> key;
+            std::memcpy(key.data(), bufs_[l].handle, 64);
+            auto it = opened_.find(key);
+            if (it == opened_.end()) {
+                hipIpcMemHandle_t handle;
+                static_assert(sizeof(handle) == 64, "IPC handle size");
+                std::memcpy(&handle, bufs_[l].handle, 64);
+                void *base = nullptr;
+                KVX_HIP(hipIpcOpenMemHandle(&base, handle, hipIpcMemLazyEnablePeerAccess));
+                // The mapping's own size bounds every access (the peer's word is not trusted).
+                void *range_base = nullptr;
+                size_t size = 0;
+                const hipError_t e = hipMemGetAddressRange(&range_base, &size, base);
+                if (e != hipSuccess) {
+                    (void)hipIpcCloseMemHandle(base);
+                    return kvx::hip_fail(e, "hipMemGetAddressRange(opened IPC buffer)", __FILE__, __LINE__);
+                }
+                it = opened_.emplace(key, Mapping{base, static_cast<int64_t>(size)}).first;
+            }
+            const int64_t need = bufs_[l].offset + static_cast<int64_t>(h.num_blocks) * g.block_stride;
+            if (bufs_[l].offset < 0 || h.num_blocks < 1 || need > it->second.bytes)
+                return kvx::fail(KV_EINVAL, "tier: layer %d (offset %lld, %d blocks of %lld bytes) exceeds its shared "
+                                            "allocation of %lld bytes",
+                                 l, static_cast<long long>(bufs_[l].offset), h.num_blocks,
+                                 static_cast<long long>(g.block_stride), static_cast<long long>(it->second.bytes));
+            layers_[static_cast<size_t>(l)] = static_cast<uint8_t *>(it->second.base) + bufs_[l].offset;
+        }
+
+        // The block table into device memory on this connection's stream.
+        const size_t table_bytes = table_host_.size() * sizeof(int32_t);
+        if (table_bytes > table_cap_) {
+            if (table_)
+                KVX_HIP(hipFree(table_));
+            table_ = nullptr;
+            table_cap_ = 0;
+            KVX_HIP(hipMalloc(reinterpret_cast<void **>(&table_), table_bytes));
+            table_cap_ = table_bytes;
+        }
+        KVX_HIP(hipMemcpyAsync(table_, table_host_.data(), table_bytes, hipMemcpyHostToDevice, stream_));
+
+        kv_cache cache;
+        std::memset(&cache, 0, sizeof(cache));
+        cache.layout = lay;
+        cache.num_blocks = h.num_blocks;
+        cache.device = pool_->device;
+        cache.block_order = h.block_order;
+        cache.layer_ptrs = layers_.data();
+        cache.block_stride_bytes = h.block_stride_bytes;
+
+        (void)kv_pool_async_error(pool_, 1);
+        kv_status st = h.op == kOpStore ? kv_store(&cache, table_, h.n_tokens, pool_, ids_.data(), stream_)
+                                        : kv_load(&cache, table_, h.n_tokens, pool_, ids_.data(), stream_);
+        const std::string enqueue_error = st != KV_OK ? std::string(kv_last_error()) : std::string();
+        // Complete whatever was enqueued before replying (the host-side completion).
+        const hipError_t e = hipStreamSynchronize(stream_);
+        if (st != KV_OK) {
+            kvx::set_last_error(enqueue_error);
+            return st;
+        }
+        if (e != hipSuccess)
+            return kvx::hip_fail(e, "hipStreamSynchronize(tier)", __FILE__, __LINE__);
+        const int32_t async = kv_pool_async_error(pool_, 1);
+        if (async != 0)
+            return kvx::fail(KV_EASYNC, "tier: device-side fault 0x%x in this request (a block id was outside "
+                                        "the cache)", static_cast<unsigned>(async));
+        return KV_OK;
+    }
+
+    kv_pool *pool_;
+    int fd_;
+    hipStream_t stream_ = nullptr;
+    int32_t *table_ = nullptr;
+    size_t table_cap_ = 0;
+    struct Mapping {
+        void *base;
+        int64_t bytes;
+    };
+    std::map<std::array<uint8_t, 64>, Mapping> opened_;
+    std::vector<kv_ipc_buffer> bufs_;
+    std::vector<int32_t> table_host_;
+    std::vector<int64_t> ids_;
+    std::vector<void *> layers_;
+};
+
+kv_status tier_request(uint32_t op, int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
+                       const int64_t *chunk_ids, void *stream) {
+    if (!cache)
+        return kvx::fail(KV_EINVAL, "cache must not be NULL");
+    kv_status st = kvx::check_layout(cache->layout);
+    if (st != KV_OK)
+        return st;
+    if (n_tokens < 0)
+        return kvx::fail(KV_EINVAL, "n_tokens must be >= 0 (got %lld)", static_cast<long long>(n_tokens));
+    if (n_tokens == 0)
+        return KV_OK;
+    if (!block_table || !chunk_ids || !cache->layer_ptrs)
+        return kvx::fail(KV_EINVAL, "block_table, chunk_ids and layer_ptrs must not be NULL for n_tokens > 0");
+    const int32_t L = cache->layout.num_layers;
+    if (L > kMaxLayers)
+        return kvx::fail(KV_EUNSUPPORTED, "more than %d layers", kMaxLayers);
+
+    // Host-side completion of everything enqueued before the call (Sec. 3.2).
+    KVX_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+
+    RequestHeader h;
+    std::memset(&h, 0, sizeof(h));
+    h.magic = kMagic;
+    h.op = op;
+    h.layout = cache->layout;
+    h.num_blocks = cache->num_blocks;
+    h.block_order = cache->block_order;
+    h.num_layers = L;
+    h.block_stride_bytes = cache->block_stride_bytes;
+    h.n_tokens = n_tokens;
+    h.n_table = ceil_div(n_tokens, cache->layout.block_size);
+    h.n_chunks = ceil_div(n_tokens, cache->layout.chunk_tokens);
+    std::vector<kv_ipc_buffer> bufs(static_cast<size_t>(L));
+    for (int32_t l = 0; l < L; ++l) {
+        st = kv_ipc_export(cache->layer_ptrs[l], &bufs[static_cast<size_t>(l)]);
+        if (st != KV_OK)
+            return st;
+    }
+    if (!write_full(fd, &h, sizeof(h)) || !write_full(fd, bufs.data(), bufs.size() * sizeof(kv_ipc_buffer)) ||
+        !write_full(fd, block_table, static_cast<size_t>(h.n_table) * sizeof(int32_t)) ||
+        !write_full(fd, chunk_ids, static_cast<size_t>(h.n_chunks) * sizeof(int64_t)))
+        return kvx::fail(KV_EINVAL, "tier connection failed while sending (%s)", std::strerror(errno));
+    ReplyHeader r;
+    if (!read_full(fd, &r, sizeof(r)) || r.magic != kMagic || r.msg_len > (1u << 20))
+        return kvx::fail(KV_EINVAL, "tier connection failed while waiting for the reply");
+    std::string msg(r.msg_len, '\0');
+    if (r.msg_len && !read_full(fd, &msg[0], r.msg_len))
+        return kvx::fail(KV_EINVAL, "tier connection failed while reading the reply");
+    if (r.status != KV_OK)
+        kvx::set_last_error("tier: " + msg);
+    return r.status;
+}
+
+}  // namespace
+
+extern "C" {
+
+kv_status kv_ipc_export(const void *dev_ptr, kv_ipc_buffer *out) {
+    if (!dev_ptr || !out)
+        return kvx::fail(KV_EINVAL, "dev_ptr and out must not be NULL");
+    void *base = nullptr;
+    size_t size = 0;
+    KVX_HIP(hipMemGetAddressRange(&base, &size, const_cast<void *>(dev_ptr)));
+    if (static_cast<int64_t>(size) >= KV_IPC_MAX_ALLOCATION_BYTES)
+        return kvx::fail(KV_EUNSUPPORTED,
+                         "allocation of %zu bytes is too large to share between processes (limit %lld); allocate "
+                         "each shared buffer separately",
+                         size, static_cast<long long>(KV_IPC_MAX_ALLOCATION_BYTES));
+    hipIpcMemHandle_t handle;
+    KVX_HIP(hipIpcGetMemHandle(&handle, base));
+    static_assert(sizeof(handle) == sizeof(out->handle), "IPC handle size");
+    std::memcpy(out->handle, &handle, sizeof(handle));
+    out->offset = static_cast<const uint8_t *>(dev_ptr) - static_cast<uint8_t *>(base);
+    out->allocation_bytes = static_cast<int64_t>(size);
+    return KV_OK;
+}
+
+kv_status kv_tier_serve(kv_pool *pool, int fd) {
+    if (!pool || fd < 0)
+        return kvx::fail(KV_EINVAL, "pool must not be NULL and fd must be a connected socket");
+    Connection c(pool, fd);
+    return c.serve();
+}
+
+kv_status kv_tier_store(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
+                        const int64_t *chunk_ids, void *stream) {
+    return tier_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, stream);
+}
+
+kv_status kv_tier_load(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
+                       const int64_t *chunk_ids, void *stream) {
+    return tier_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, stream);
+}
+
+}  // extern "C"

@@ -87,6 +87,10 @@ class KvIndexStats(ctypes.Structure):
                                                       "free_state_slots", "evictions", "state_evictions")]
 
 
+class KvIpcBuffer(ctypes.Structure):
+    _fields_ = [("handle", ctypes.c_uint8 * 64), ("offset", ctypes.c_int64), ("allocation_bytes", ctypes.c_int64)]
+
+
 class KvError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(message)
@@ -126,6 +130,10 @@ def _open():
         "kv_index_reserve_state": ([P, i64, ctypes.POINTER(i64), ctypes.POINTER(i32)], i32),
         "kv_index_commit_state": ([P, i64, ctypes.c_int], i32),
         "kv_index_get_stats": ([P, ctypes.POINTER(KvIndexStats)], i32),
+        "kv_ipc_export": ([P, ctypes.POINTER(KvIpcBuffer)], i32),
+        "kv_tier_serve": ([P, ctypes.c_int], i32),
+        "kv_tier_store": ([ctypes.c_int, ctypes.POINTER(KvCache), P, i64, P, P], i32),
+        "kv_tier_load": ([ctypes.c_int, ctypes.POINTER(KvCache), P, i64, P, P], i32),
         "kv_last_error": ([], ctypes.c_char_p),
         "kv_status_name": ([i32], ctypes.c_char_p),
         "kv_version": ([], ctypes.c_char_p),
@@ -144,7 +152,8 @@ EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slo
            "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version", "kv_pool_state_slot",
            "kv_check_state", "kv_store_state", "kv_load_state", "kv_index_create", "kv_index_destroy",
            "kv_index_keys", "kv_index_lookup", "kv_index_unpin", "kv_index_reserve", "kv_index_commit",
-           "kv_index_reserve_state", "kv_index_commit_state", "kv_index_get_stats")
+           "kv_index_reserve_state", "kv_index_commit_state", "kv_index_get_stats", "kv_ipc_export",
+           "kv_tier_serve", "kv_tier_store", "kv_tier_load")
 
 
 def kv_last_error() -> str:
@@ -491,3 +500,42 @@ def kv_index_get_stats(index: Index) -> dict:
     st = KvIndexStats()
     _raise(_lib.kv_index_get_stats(index.handle, ctypes.byref(st)))
     return {name: int(getattr(st, name)) for name, _ in KvIndexStats._fields_}
+
+
+# ---- Tier: a pool shared by replicas in other processes ----------------------------------
+
+KV_IPC_MAX_ALLOCATION_BYTES = 2 << 30
+
+
+def kv_ipc_export(ptr) -> KvIpcBuffer:
+    """IPC buffer of a device pointer (int or tensor) of this process."""
+    out = KvIpcBuffer()
+    p = ptr.data_ptr() if isinstance(ptr, torch.Tensor) else int(ptr)
+    _raise(_lib.kv_ipc_export(ctypes.c_void_p(p), ctypes.byref(out)))
+    return out
+
+
+def kv_tier_serve(pool: Pool, fd: int) -> None:
+    """Serve one replica connection on the connected stream socket ``fd`` until it closes (blocks;
+    the GIL is released while it runs)."""
+    _raise(_lib.kv_tier_serve(pool.handle, int(fd)))
+
+
+def _host_table(block_table):
+    t = np.ascontiguousarray(np.asarray(block_table, dtype=np.int32))
+    return t, (ctypes.c_void_p(t.ctypes.data) if t.size else None)
+
+
+def kv_tier_store(fd: int, cache: Cache, block_table, n_tokens: int, chunk_ids, stream=None) -> None:
+    """Store through the tier on ``fd``: ``block_table`` is a HOST int32 array; ``stream`` is
+    synchronised first; returns once the tier has committed the chunks."""
+    t, tp = _host_table(block_table)
+    ids, ip = _chunk_ids(chunk_ids)
+    _raise(_lib.kv_tier_store(int(fd), ctypes.byref(cache.struct), tp, int(n_tokens), ip, _stream_handle(stream)))
+
+
+def kv_tier_load(fd: int, cache: Cache, block_table, n_tokens: int, chunk_ids, stream=None) -> None:
+    """Load through the tier on ``fd`` into ``cache``; returns once the cache is complete."""
+    t, tp = _host_table(block_table)
+    ids, ip = _chunk_ids(chunk_ids)
+    _raise(_lib.kv_tier_load(int(fd), ctypes.byref(cache.struct), tp, int(n_tokens), ip, _stream_handle(stream)))

@@ -1,0 +1,146 @@
+"""Two replica processes share one pool through a tier process (the paper's shared host tier,
+Sec. 2 and Fig. 1), with the host-side completion handshake of Sec. 3.2.
+
+Three processes on the GPU: the tier owns the pinned pool; replica A (a child process) stores
+its prefix through the tier; replica B (this test) loads it into a fresh fragmented block set.
+The pool bytes (dumped by the tier) and B's cache are compared with the oracle.
+"""
+import os
+import socket
+import subprocess
+import sys
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import harness
+from paper_2609_15021_amd import kvx
+from tests.gpu_support import DEV, TINY, first_mismatch, host_cache, oracle_pool, oracle_unpack_into, to_host
+
+pytestmark = pytest.mark.gpu
+
+ROLES = os.path.join(os.path.dirname(os.path.abspath(__file__)), "tier_roles.py")
+POOL_SENT = 0xA5
+
+
+def _dims(lay):
+    return [str(v) for v in (lay.L, lay.H, lay.D, lay.E, lay.BS, lay.C)]
+
+
+def _start_tier(sock, lay, slots, mode, nconn, dump):
+    p = subprocess.Popen([sys.executable, "-u", ROLES, "tier", sock, *_dims(lay), str(slots), mode, str(nconn), dump],
+                         stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    t0 = time.time()
+    while time.time() - t0 < 90:
+        line = p.stdout.readline()
+        if line.startswith("READY"):
+            return p
+        if not line and p.poll() is not None:
+            break
+    p.kill()
+    raise AssertionError(f"tier did not start: {p.stdout.read()[-2000:]}")
+
+
+def _finish_tier(p):
+    out, _ = p.communicate(timeout=90)
+    assert p.returncode == 0, out[-2000:]
+    line = [ln for ln in out.splitlines() if ln.startswith("TIER")][-1]
+    assert set(line.split(" ", 1)[1].split(";")) == {"ok"}, line
+
+
+def _store_process(sock, lay, NB, n, seed, delay_ms):
+    r = subprocess.run([sys.executable, "-u", ROLES, "store", sock, *_dims(lay), str(NB), str(n), str(seed),
+                        str(delay_ms)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and "STORED" in r.stdout, (r.stdout + r.stderr)[-3000:]
+
+
+def _connect(sock):
+    c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    c.connect(sock)
+    return c
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_two_replica_processes_share_one_pool(mode, tmp_path):
+    lay = TINY
+    n = 3 * lay.C + 100
+    nc, NB = lay.nc(n), lay.nblk(n) + 9
+    seed = harness.sub_seed("tier", mode)
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    tier = _start_tier(sock, lay, nc + 2, mode, 2, dump)
+    try:
+        _store_process(sock, lay, NB, n, seed, 0)
+        btB = harness.block_table(seed + 2, NB, lay.nblk(n))
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
+        s = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        c = _connect(sock)
+        kvx.kv_tier_load(c.fileno(), kvx.Cache(dB, lay.kv, NB), btB, n, np.arange(nc), s)
+        got_B = dB.cpu()  # the load completed before kv_tier_load returned
+        c.close()
+    finally:
+        _finish_tier(tier)
+    A = host_cache(lay, NB, seed, "raw")
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+    want_pool = oracle_pool(lay, A, btA, n, np.arange(nc), nc + 2, POOL_SENT)
+    pool = np.load(dump)
+    assert np.array_equal(pool, want_pool), first_mismatch(pool, want_pool)
+    want_B = oracle_unpack_into(lay, np.zeros_like(A), btB, n, want_pool, np.arange(nc))
+    got = got_B.numpy().view(A.dtype).reshape(A.shape)
+    assert np.array_equal(got, want_B), first_mismatch(got, want_B)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_delayed_producer_across_processes(mode, tmp_path):
+    """Replica A's producer writes byte 37 after a 60 ms spin on its stream; the store request
+    leaves A only after that stream completed, so every committed byte is 37 (Sec. 3.2)."""
+    lay = TINY
+    n = 1024
+    nc, NB = lay.nc(n), lay.nblk(n) + 4
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    tier = _start_tier(sock, lay, nc, mode, 1, dump)
+    try:
+        _store_process(sock, lay, NB, n, harness.sub_seed("tier-37", mode), 60)
+    finally:
+        _finish_tier(tier)
+    pool = np.load(dump)
+    assert pool.size == nc * lay.slot_bytes and (pool == 37).all()
+
+
+def test_tier_rejects_a_bad_request_and_keeps_serving(tmp_path):
+    lay = TINY
+    n = 512
+    nc, NB = lay.nc(n), 64
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    tier = _start_tier(sock, lay, nc, "staged", 1, dump)
+    try:
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
+        cache = kvx.Cache(dB, lay.kv, NB)
+        bt = np.arange(lay.nblk(n), dtype=np.int32)
+        c = _connect(sock)
+        with pytest.raises(kvx.KvError) as e:
+            kvx.kv_tier_load(c.fileno(), cache, bt, n, [0, nc], None)   # chunk id outside the pool
+        assert e.value.status == kvx.KV_EINVAL and "tier:" in str(e.value)
+        big = kvx.Cache(dB, lay.kv, NB)
+        big.struct.num_blocks = 10000                                 # claims more than B's allocation
+        with pytest.raises(kvx.KvError) as e:
+            kvx.kv_tier_load(c.fileno(), big, bt, n, np.arange(nc), None)
+        assert e.value.status == kvx.KV_EINVAL and "exceeds its shared allocation" in str(e.value)
+        kvx.kv_tier_load(c.fileno(), cache, bt, n, np.arange(nc), None)  # still served
+        c.close()
+    finally:
+        _finish_tier(tier)
+
+
+def test_ipc_export_refuses_allocations_of_2_gib():
+    t = torch.empty(2 << 30, dtype=torch.uint8, device=DEV)
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_ipc_export(t)
+    assert e.value.status == kvx.KV_EUNSUPPORTED
+    small = torch.empty(1 << 20, dtype=torch.uint8, device=DEV)
+    buf = kvx.kv_ipc_export(small[4096:])
+    assert buf.allocation_bytes < (2 << 30) and buf.offset >= 4096
+    del t
+    torch.cuda.empty_cache()

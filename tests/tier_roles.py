@@ -1,0 +1,88 @@
+"""Process roles for the tier tests (run as separate processes by tests/test_gpu_tier.py).
+
+  tier  SOCK L H D E BS C SLOTS MODE NCONN DUMP   own the pool, serve NCONN replica connections,
+                                                  then save the pool bytes to DUMP
+  store SOCK L H D E BS C NB N SEED DELAY_MS      replica A: its cache from the seeded generator
+                                                  (DELAY_MS > 0: zeros, then a delayed producer
+                                                  writes byte 37 on its stream), stored through the tier
+"""
+import os
+import socket
+import sys
+import threading
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+import harness  # noqa: E402
+from harness import gpu as hg  # noqa: E402
+from paper_2609_15021_amd import kvx  # noqa: E402
+
+POOL_SENT = 0xA5
+
+
+def tier(sock, L, H, D, E, BS, C, slots, mode, nconn, dump):
+    lay = kvx.make_layout(L, H, D, E, BS, C)
+    pool = kvx.kv_pool_create(lay, slots, mode, staging_slots=2, chunks_per_batch=2)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    srv = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    srv.bind(sock)
+    srv.listen(8)
+    srv.settimeout(90)
+    print("READY", flush=True)
+    results = []
+
+    def serve(conn):
+        try:
+            kvx.kv_tier_serve(pool, conn.fileno())
+            results.append("ok")
+        except Exception as e:  # reported to the test through stdout
+            results.append(repr(e))
+        finally:
+            conn.close()
+
+    threads = []
+    for _ in range(nconn):
+        conn, _ = srv.accept()
+        t = threading.Thread(target=serve, args=(conn,))
+        t.start()
+        threads.append(t)
+    for t in threads:
+        t.join(timeout=90)
+    np.save(dump, view.copy())
+    print("TIER", ";".join(results), flush=True)
+    kvx.kv_pool_destroy(pool)
+
+
+def store(sock, L, H, D, E, BS, C, NB, n, seed, delay_ms):
+    lay = kvx.make_layout(L, H, D, E, BS, C)
+    A = harness.gen_cache(seed, "raw", L, NB, H, BS, D, E)
+    dA = torch.from_numpy(A.view({1: np.uint8, 2: np.int16, 4: np.int32}[E])).to("cuda:0")
+    bt = harness.block_table(seed + 1, NB, -(-n // BS))
+    ids = np.arange(-(-n // C))
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    if delay_ms > 0:
+        dA.zero_()
+        torch.cuda.synchronize()
+        hg.spin(float(delay_ms), s)
+        hg.fill_u8(dA, dA.numel() * dA.element_size(), 37, s)
+    c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    c.connect(sock)
+    kvx.kv_tier_store(c.fileno(), kvx.Cache(dA, lay, NB), bt, n, ids, s)
+    c.close()
+    print("STORED", flush=True)
+
+
+if __name__ == "__main__":
+    role, args = sys.argv[1], sys.argv[2:]
+    if role == "tier":
+        tier(args[0], *map(int, args[1:8]), args[8], int(args[9]), args[10])
+    elif role == "store":
+        store(args[0], *map(int, args[1:12]))
+    else:
+        raise SystemExit(f"unknown role {role}")

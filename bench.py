@@ -16,8 +16,8 @@ host-link rate against the measured pinned-copy peak, a zero-copy comparison,
 a sampled round-trip check against the seeded generator, and the CPU oracle's
 own throughput on a bounded sample (the cpu_baseline; the only use of the
 oracle here).  Side legs: the paper-native attention layout, recurrent-state
-snapshot pages of a hybrid model, and the host-side pool index at the paper's
-256 GiB tier size.
+snapshot pages of a hybrid model, store/restore between processes through a
+tier process, and the host-side pool index at the paper's 256 GiB tier size.
 """
 from __future__ import annotations
 
@@ -62,6 +62,11 @@ def parse():
     ap.add_argument("--state-only", action="store_true",
                     help="only measure recurrent-state snapshots and print its JSON object (run by the main bench)")
     ap.add_argument("--no-index", action="store_true", help="skip the pool-index measurement")
+    ap.add_argument("--no-tier", action="store_true", help="skip the cross-process (tier) measurement")
+    ap.add_argument("--tier-only", action="store_true",
+                    help="only measure store/restore between processes through a tier (run by the main bench)")
+    ap.add_argument("--tier-server", metavar="SOCKET", help=argparse.SUPPRESS)
+    ap.add_argument("--tier-store", metavar="SOCKET", help=argparse.SUPPRESS)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (PMC counter scale reference)")
     return ap.parse_args()
@@ -350,6 +355,134 @@ def pool_index_oracle(np, model_cls, prompts):
             "sample": f"the first {done} requests of the pool-index stream, single thread"}
 
 
+TIER_N, TIER_NB = 131072, 10240
+
+
+def layer_caches(torch, hg, kvx, nb, dev, seed=None):
+    """A replica cache as one device allocation per layer (each < 2 GiB, shareable by IPC); with a
+    seed, filled with the generator's values of the layer-stacked cache."""
+    layers = [torch.empty((nb, 2, H, BS, D), dtype=torch.int16, device=dev) for _ in range(L)]
+    for l, t in enumerate(layers):
+        if seed is None:
+            t.zero_()
+        else:
+            hg.fill_values(t, l * nb * 2 * H * BS * D, seed, "n01", E)
+    torch.cuda.synchronize()
+    return layers, kvx.Cache(layers, kvx.make_layout(L, H, D, E, BS, C), nb)
+
+
+def tier_server(torch, kvx, sock, mode):
+    import socket
+    import threading
+    pool = kvx.kv_pool_create(kvx.make_layout(L, H, D, E, BS, C), -(-TIER_N // C), mode, profile=True)
+    srv = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    srv.bind(sock)
+    srv.listen(4)
+    srv.settimeout(300)
+    print("READY", flush=True)
+    errors = []
+
+    def serve(conn):
+        try:
+            kvx.kv_tier_serve(pool, conn.fileno())
+        except Exception as e:  # reported through stdout
+            errors.append(repr(e))
+        finally:
+            conn.close()
+
+    threads = []
+    for _ in range(2):  # replica A, then replica B
+        conn, _ = srv.accept()
+        threads.append(threading.Thread(target=serve, args=(conn,)))
+        threads[-1].start()
+    for t in threads:
+        t.join()
+    kern = {}
+    for w in ("pack", "unpack"):
+        n, ms, alg = kvx.kv_pool_kernel_stats(pool, w)
+        if n:
+            kern[w] = {"launches": n, "avg_launch_ms": round(ms / n, 4),
+                       "achieved_GBps": round(alg / (ms / 1e3) / 1e9, 1)}
+    kvx.kv_pool_destroy(pool)
+    print(json.dumps({"errors": errors, "kernels": kern}), flush=True)
+    sys.exit(1 if errors else 0)
+
+
+def tier_store(np, torch, harness, hg, kvx, sock, dev):
+    import socket
+    seed = harness.sub_seed("bench-tier", TIER_N)
+    _, cache = layer_caches(torch, hg, kvx, TIER_NB, dev, seed)
+    bt = harness.block_table(seed + 1, TIER_NB, TIER_N // BS)
+    c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    c.connect(sock)
+    t0 = time.perf_counter()
+    kvx.kv_tier_store(c.fileno(), cache, bt, TIER_N, np.arange(TIER_N // C))
+    dt = time.perf_counter() - t0
+    c.close()
+    print(json.dumps({"store_s": dt}), flush=True)
+
+
+def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
+    """Replica A (a process) stores a 128k prefix through a tier process that owns the pool;
+    replica B (this process) restores it: host wall clock of each request, handshake included."""
+    import socket
+    import subprocess
+    import tempfile
+    tmp = tempfile.mkdtemp(prefix="kvx_tier_")
+    sock = os.path.join(tmp, "tier.sock")
+    me = os.path.abspath(__file__)
+    tier = subprocess.Popen([sys.executable, "-u", me, "--tier-server", sock, "--mode", mode],
+                            stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+    try:
+        line = tier.stdout.readline()
+        if not line.startswith("READY"):
+            raise RuntimeError("tier did not start: " + tier.stderr.read()[-2000:])
+        r = subprocess.run([sys.executable, "-u", me, "--tier-store", sock], capture_output=True, text=True,
+                           timeout=300)
+        if r.returncode != 0:
+            raise RuntimeError("replica A failed: " + r.stderr[-2000:])
+        store_s = json.loads(r.stdout.strip().splitlines()[-1])["store_s"]
+        seed = harness.sub_seed("bench-tier", TIER_N)
+        layers_b, cache_b = layer_caches(torch, hg, kvx, TIER_NB, dev)
+        bt_a = harness.block_table(seed + 1, TIER_NB, TIER_N // BS)
+        bt_b = harness.block_table(seed + 2, TIER_NB, TIER_N // BS)
+        c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+        c.connect(sock)
+        restore = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            kvx.kv_tier_load(c.fileno(), cache_b, bt_b, TIER_N, np.arange(TIER_N // C))
+            restore.append(time.perf_counter() - t0)
+        c.close()
+        out, err = tier.communicate(timeout=120)
+        if tier.returncode != 0:
+            raise RuntimeError("tier failed: " + (out + err)[-2000:])
+        kern = json.loads(out.strip().splitlines()[-1])["kernels"]
+    finally:
+        if tier.poll() is None:
+            tier.kill()
+    class PerLayer:  # indexes per-layer buffers as the sampled check indexes a stacked cache
+        def __init__(self, layers):
+            self.layers, self.device = layers, layers[0].device
+
+        def __getitem__(self, key):
+            return torch.stack([t[key[1]] for t in self.layers])
+
+    stacked = type("Stacked", (), {})()
+    stacked.t = PerLayer(layers_b)
+    nc = TIER_N // C
+    ok, msg = sampled_round_trip(np, harness, stacked, bt_a, bt_b, seed, TIER_N, TIER_NB, [0, nc // 2, nc - 1],
+                                 torch)
+    N = TIER_N * TOKEN_BYTES
+    return {"workload": "replica A (a process) stores the 131,072-token 27B-class prefix through a tier process "
+                        "that owns the pinned pool; replica B (another process) restores it; caches shared by HIP "
+                        "IPC, one allocation per layer; host-side completion at both ends",
+            "mode": mode, "store_s": round(store_s, 4), "store_GBps": round(N / store_s / 1e9, 3),
+            "restore_s_first": round(restore[0], 4), "restore_s": round(statistics.median(restore[1:] or restore), 4),
+            "restore_GBps": round(N / statistics.median(restore[1:] or restore) / 1e9, 3),
+            "tier_kernels": kern, "round_trip": msg if ok else f"FAILED: {msg}"}, ok
+
+
 def cpu_baseline(np, oracle, n_chunks=64):
     """The oracle timed on host cores: store + load of a bounded sample of the workload."""
     rng = np.random.default_rng(2609)
@@ -408,6 +541,22 @@ def main():
         res, res_ok = state_snapshots(np, torch, hg, kvx, args.mode, dev)
         print(json.dumps(res), flush=True)
         sys.exit(0 if res_ok else 1)
+    if args.tier_server:
+        tier_server(torch, kvx, args.tier_server, args.mode)
+        return
+    if args.tier_store:
+        tier_store(np, torch, harness, hg, kvx, args.tier_store, dev)
+        return
+    if args.tier_only:
+        # Both modes: across processes zero-copy was measured faster than staged (the staged
+        # host-to-device copies slow down while kernels write IPC-imported caches).
+        res, res_ok = {}, True
+        for mode in ("zero_copy", "staged"):
+            r, ok_m = tier_leg(np, torch, harness, hg, kvx, mode, dev)
+            res[mode] = r
+            res_ok = res_ok and ok_m
+        print(json.dumps(res), flush=True)
+        sys.exit(0 if res_ok else 1)
 
     # The side legs run first, each in its own process, on fresh memory: on these machines,
     # transfers through pools created after large allocations were freed measured ~10% slower
@@ -432,7 +581,15 @@ def main():
         if "error" not in state:
             log(f"[bench] state snapshots: store {state['store_GBps']} GB/s, load {state['load_GBps']} GB/s, "
                 f"kernels {json.dumps(state['kernels'])}; {state['round_trip']}")
-    paper_ok = paper_ok and state_ok
+    tier, tier_ok = None, True
+    if not args.no_tier:
+        tier, tier_ok = child_leg("--tier-only")
+        if "error" not in tier:
+            for m, t in tier.items():
+                log(f"[bench] tier ({m}, 3 processes): store {t['store_s']} s ({t['store_GBps']} GB/s), restore "
+                    f"{t['restore_s']} s ({t['restore_GBps']} GB/s, first {t['restore_s_first']} s); "
+                    f"{t['round_trip']}")
+    paper_ok = paper_ok and state_ok and tier_ok
 
     layout = kvx.make_layout(L, H, D, E, BS, C)
     n = args.tokens
@@ -627,6 +784,7 @@ def main():
         "parity_256k": parity_256k,
         "paper_layout": paper,
         "state_snapshots": state,
+        "tier": tier,
         "pool_index": index,
         "cpu_baseline": cpu,
     }

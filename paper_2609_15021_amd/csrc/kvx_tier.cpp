@@ -105,6 +105,8 @@ class Connection {
             (void)hipIpcCloseMemHandle(kv.second.base);
         if (table_)
             (void)hipFree(table_);
+        if (table_pinned_)
+            (void)hipHostFree(table_pinned_);
     }
 
     kv_status serve() {
@@ -194,17 +196,23 @@ class Connection {
             layers_[static_cast<size_t>(l)] = static_cast<uint8_t *>(it->second.base) + bufs_[l].offset;
         }
 
-        // The block table into device memory on this connection's stream.
+        // The block table into device memory on this connection's stream, from pinned host
+        // memory (an asynchronous copy from pageable memory would take the runtime's staged path).
         const size_t table_bytes = table_host_.size() * sizeof(int32_t);
         if (table_bytes > table_cap_) {
             if (table_)
                 KVX_HIP(hipFree(table_));
+            if (table_pinned_)
+                KVX_HIP(hipHostFree(table_pinned_));
             table_ = nullptr;
+            table_pinned_ = nullptr;
             table_cap_ = 0;
             KVX_HIP(hipMalloc(reinterpret_cast<void **>(&table_), table_bytes));
+            KVX_HIP(hipHostMalloc(reinterpret_cast<void **>(&table_pinned_), table_bytes, hipHostMallocDefault));
             table_cap_ = table_bytes;
         }
-        KVX_HIP(hipMemcpyAsync(table_, table_host_.data(), table_bytes, hipMemcpyHostToDevice, stream_));
+        std::memcpy(table_pinned_, table_host_.data(), table_bytes);
+        KVX_HIP(hipMemcpyAsync(table_, table_pinned_, table_bytes, hipMemcpyHostToDevice, stream_));
 
         kv_cache cache;
         std::memset(&cache, 0, sizeof(cache));
@@ -238,6 +246,7 @@ class Connection {
     int fd_;
     hipStream_t stream_ = nullptr;
     int32_t *table_ = nullptr;
+    int32_t *table_pinned_ = nullptr;  // host staging of the table (the previous request has completed)
     size_t table_cap_ = 0;
     struct Mapping {
         void *base;

@@ -144,3 +144,32 @@ def test_ipc_export_refuses_allocations_of_2_gib():
     assert buf.allocation_bytes < (2 << 30) and buf.offset >= 4096
     del t
     torch.cuda.empty_cache()
+
+
+def test_tier_survives_a_malformed_connection(tmp_path):
+    """A connection that sends a garbage frame ends with an error on its own; the tier keeps serving
+    the next replica."""
+    lay = TINY
+    n = 512
+    nc, NB = lay.nc(n), 64
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    p = subprocess.Popen([sys.executable, "-u", ROLES, "tier", sock, *_dims(lay), str(nc), "staged", "2", dump],
+                         stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    try:
+        assert p.stdout.readline().startswith("READY")
+        bad = _connect(sock)
+        bad.sendall(b"\x00" * 160)  # a full header's worth of bytes with the wrong magic
+        bad.close()
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
+        c = _connect(sock)
+        kvx.kv_tier_load(c.fileno(), kvx.Cache(dB, lay.kv, NB), np.arange(lay.nblk(n), dtype=np.int32), n,
+                         np.arange(nc), None)
+        c.close()
+        out, _ = p.communicate(timeout=90)
+    finally:
+        if p.poll() is None:
+            p.kill()
+    assert p.returncode == 0, out[-2000:]
+    results = [ln for ln in out.splitlines() if ln.startswith("TIER")][-1].split(" ", 1)[1].split(";")
+    assert sorted(r == "ok" for r in results) == [False, True], results
+    assert any("malformed" in r for r in results), results

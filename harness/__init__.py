@@ -150,3 +150,9 @@ def chunk_ids(n_chunks: int, num_slots: int, seed=None, first: int = 0) -> np.nd
 def spin_delays_ms(seed: int, count: int, lo: float = 5.0, hi: float = 50.0) -> np.ndarray:
     """Seeded producer delays in [lo, hi] milliseconds."""
     return np.random.default_rng(seed).uniform(lo, hi, size=count)
+
+
+def prompt_tokens(seed: int, n: int, vocab: int = 151000) -> np.ndarray:
+    """A seeded synthetic prompt of n token ids (int32); prompts sharing a prefix come from
+    slicing or concatenating these."""
+    return np.random.default_rng(seed).integers(0, vocab, size=n).astype(np.int32)

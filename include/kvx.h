@@ -432,10 +432,21 @@ KV_API kv_status kv_ipc_export(const void *dev_ptr, kv_ipc_buffer *out);
 
 /* Serve one replica connection: read requests from the connected stream socket
  * `fd` until the peer closes it, run each on `pool` (current device = the
- * pool's), reply.  Blocks.  Returns KV_OK on an orderly close, an error if the
- * connection failed or sent a malformed frame (then the socket is left open
+ * pool's), reply.  `index` (may be NULL) manages the pool's slots for the
+ * prefix requests below; it must cover at most the pool's slots and use the
+ * pool's chunk length.  Blocks.  Returns KV_OK on an orderly close, an error
+ * if the connection failed or sent a malformed frame (the socket is left open
  * for the caller to close). */
-KV_API kv_status kv_tier_serve(kv_pool *pool, int fd);
+KV_API kv_status kv_tier_serve(kv_pool *pool, kv_index *index, int fd);
+
+/* A listening stream socket at filesystem path `path` (which must not exist yet):
+ * *listen_fd receives it.  KV_EINVAL on failure (reason in kv_last_error). */
+KV_API kv_status kv_tier_listen(const char *path, int *listen_fd);
+
+/* Accept `connections` replica connections on listen_fd (0 = until the listening
+ * socket fails), serve each on its own thread as kv_tier_serve does, close them,
+ * and return when all have ended: KV_OK, or the first connection's error. */
+KV_API kv_status kv_tier_run(kv_pool *pool, kv_index *index, int listen_fd, int32_t connections);
 
 /* Replica side.  cache: this process's cache (layer pointers are exported);
  * block_table: HOST int32[ceil(n_tokens / BS)], read before return; chunk_ids:
@@ -447,6 +458,23 @@ KV_API kv_status kv_tier_store(int fd, const kv_cache *cache, const int32_t *blo
                                const int64_t *chunk_ids, void *stream);
 KV_API kv_status kv_tier_load(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                               const int64_t *chunk_ids, void *stream);
+
+/* Prefix requests (a tier served with an index): the replica names its prompt
+ * (tokens: HOST int32[n_tokens], cache salt) and the tier picks the slots.
+ *   kv_tier_store_prefix: reserve the prompt's whole chunks, store those not yet
+ *     in the pool (runs of consecutive new chunks, one kv_store each; the
+ *     partial last chunk is not kept), commit them after the stores completed,
+ *     or abort them if a store failed.  *stored_chunks = chunks written.
+ *   kv_tier_load_prefix: the longest whole-chunk hit (Sec. 3.1-3.2: hits are
+ *     whole chunks), pinned while it is loaded into the cache's first
+ *     hit_tokens token slots.  *hit_tokens = hit chunks * C (0: nothing loaded).
+ * block_table: HOST int32[ceil(n_tokens / BS)] for the whole prompt.  KV_EBUSY
+ * if the index cannot free enough slots (nothing stored). */
+KV_API kv_status kv_tier_store_prefix(int fd, const kv_cache *cache, const int32_t *block_table, uint64_t salt,
+                                      const int32_t *tokens, int64_t n_tokens, int64_t *stored_chunks,
+                                      void *stream);
+KV_API kv_status kv_tier_load_prefix(int fd, const kv_cache *cache, const int32_t *block_table, uint64_t salt,
+                                     const int32_t *tokens, int64_t n_tokens, int64_t *hit_tokens, void *stream);
 
 /* Thread-local text of the last failure on this thread (HIP error name, message, call site). */
 KV_API const char *kv_last_error(void);

@@ -211,6 +211,13 @@ struct kv_index {
     }
 };
 
+namespace kvx {
+
+int32_t index_chunk_tokens(const kv_index *index) { return index->C; }
+int64_t index_num_slots(const kv_index *index) { return index->num_slots; }
+
+}  // namespace kvx
+
 namespace {
 
 kv_status check_tokens(const kv_index *x, const int32_t *tokens, int64_t n_tokens) {

@@ -104,6 +104,10 @@ kv_status check_request(const kv_cache *cache, const kv_layout *pool_layout, int
 kv_status check_state_request(const kv_state *state, int64_t pool_state_slot_bytes, int64_t pool_state_slots,
                               int64_t n, const int64_t *pages, const int64_t *slot_ids, int for_store);
 
+// Geometry of a pool index (for the tier's consistency check).
+int32_t index_chunk_tokens(const kv_index *index);
+int64_t index_num_slots(const kv_index *index);
+
 }  // namespace kvx
 
 // The pool: one pinned host region plus the staging ring and its streams/events.

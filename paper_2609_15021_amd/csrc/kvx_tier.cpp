@@ -6,18 +6,25 @@
 // registered in a second process, so the process that pinned the pool also runs every
 // copy into and out of it; replicas hand over device memory instead.  Both ends complete
 // on the host before handing over: the replica synchronises its stream before sending,
-// and the tier synchronises its own stream before replying.
+// and the tier synchronises its own stream before replying.  With an index the tier also
+// chooses the slots: prefix requests name a prompt, and the tier stores the prompt's
+// missing whole chunks or loads its longest whole-chunk hit.
 //
 // Frames are native-layout structs (both ends run on one host): a request header, the
-// layers' IPC buffers, the block table and the chunk ids; a reply header and a message.
+// layers' IPC buffers, the block table, the chunk ids and the prompt's tokens; a reply
+// header and a message.
 #include <sys/socket.h>
 #include <sys/types.h>
+#include <sys/un.h>
+#include <unistd.h>
 
 #include <array>
 #include <cerrno>
 #include <cstring>
+#include <deque>
 #include <map>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "kvx_internal.h"
@@ -25,7 +32,7 @@
 namespace {
 
 constexpr uint32_t kMagic = 0x5458564Bu;  // "KVXT"
-constexpr uint32_t kOpStore = 1, kOpLoad = 2;
+enum Op : uint32_t { kOpStore = 1, kOpLoad = 2, kOpStorePrefix = 3, kOpLoadPrefix = 4 };
 constexpr int32_t kMaxLayers = 4096;
 constexpr int64_t kMaxPayload = int64_t(1) << 30;
 
@@ -39,8 +46,10 @@ struct RequestHeader {
     int32_t pad;
     int64_t block_stride_bytes;
     int64_t n_tokens;
-    int64_t n_table;   // int32 block-table entries that follow the layers
-    int64_t n_chunks;  // int64 chunk ids that follow the table
+    int64_t n_table;   // int32 block-table entries after the layers
+    int64_t n_chunks;  // int64 chunk ids after the table (slot requests)
+    int64_t n_ids;     // int32 token ids after the chunk ids (prefix requests)
+    uint64_t salt;
 };
 
 struct ReplyHeader {
@@ -48,6 +57,7 @@ struct ReplyHeader {
     int32_t status;
     uint32_t msg_len;
     uint32_t pad;
+    int64_t value;  // chunks stored (store prefix) or tokens hit (load prefix)
 };
 
 // Whole-buffer socket I/O.  Returns false on EOF or error (errno kept); *eof set on a clean
@@ -94,7 +104,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // The tier end of one connection.
 class Connection {
   public:
-    Connection(kv_pool *pool, int fd) : pool_(pool), fd_(fd) {}
+    Connection(kv_pool *pool, kv_index *index, int fd) : pool_(pool), index_(index), fd_(fd) {}
 
     ~Connection() {
         if (stream_) {
@@ -121,51 +131,49 @@ class Connection {
                 return kvx::fail(KV_EINVAL, "tier: connection failed while reading a request (%s)",
                                  std::strerror(errno));
             }
-            if (h.magic != kMagic || (h.op != kOpStore && h.op != kOpLoad) || h.num_layers < 1 ||
-                h.num_layers > kMaxLayers || h.n_table < 0 || h.n_chunks < 0)
+            if (h.magic != kMagic || h.op < kOpStore || h.op > kOpLoadPrefix || h.num_layers < 1 ||
+                h.num_layers > kMaxLayers || h.n_table < 0 || h.n_chunks < 0 || h.n_ids < 0)
                 return kvx::fail(KV_EINVAL, "tier: malformed request header");
             const int64_t payload = static_cast<int64_t>(h.num_layers) * int64_t(sizeof(kv_ipc_buffer)) +
-                                    h.n_table * int64_t(sizeof(int32_t)) + h.n_chunks * int64_t(sizeof(int64_t));
+                                    h.n_table * int64_t(sizeof(int32_t)) + h.n_chunks * int64_t(sizeof(int64_t)) +
+                                    h.n_ids * int64_t(sizeof(int32_t));
             if (payload > kMaxPayload)
                 return kvx::fail(KV_EINVAL, "tier: request payload of %lld bytes is too large",
                                  static_cast<long long>(payload));
             bufs_.resize(static_cast<size_t>(h.num_layers));
             table_host_.resize(static_cast<size_t>(h.n_table));
             ids_.resize(static_cast<size_t>(h.n_chunks));
+            tokens_.resize(static_cast<size_t>(h.n_ids));
             if (!read_full(fd_, bufs_.data(), bufs_.size() * sizeof(kv_ipc_buffer)) ||
                 !read_full(fd_, table_host_.data(), table_host_.size() * sizeof(int32_t)) ||
-                !read_full(fd_, ids_.data(), ids_.size() * sizeof(int64_t)))
+                !read_full(fd_, ids_.data(), ids_.size() * sizeof(int64_t)) ||
+                !read_full(fd_, tokens_.data(), tokens_.size() * sizeof(int32_t)))
                 return kvx::fail(KV_EINVAL, "tier: connection failed while reading a request body");
 
             kv_status st;
+            int64_t value = 0;
             {
                 std::lock_guard<std::mutex> lock(pool_->tier_mu);
-                st = execute(h);
+                st = execute(h, &value);
             }
             const std::string msg = st == KV_OK ? std::string() : std::string(kv_last_error());
-            ReplyHeader r{kMagic, st, static_cast<uint32_t>(msg.size()), 0};
+            ReplyHeader r{kMagic, st, static_cast<uint32_t>(msg.size()), 0, value};
             if (!write_full(fd_, &r, sizeof(r)) || !write_full(fd_, msg.data(), msg.size()))
                 return kvx::fail(KV_EINVAL, "tier: connection failed while replying (%s)", std::strerror(errno));
         }
     }
 
   private:
-    kv_status execute(const RequestHeader &h) {
+    // The replica's cache as this process sees it (layers mapped once per connection, each
+    // bounded by the size of the mapping opened here), and its block table on the device.
+    kv_status map_cache(const RequestHeader &h, kv_cache *cache) {
         const kv_layout &lay = h.layout;
-        if (lay.block_size < 1 || lay.chunk_tokens < 1 || h.n_tokens < 0 || lay.num_layers != h.num_layers)
-            return kvx::fail(KV_EINVAL, "tier: request layout or length is invalid");
-        if (h.n_table != ceil_div(h.n_tokens, lay.block_size) || h.n_chunks != ceil_div(h.n_tokens, lay.chunk_tokens))
-            return kvx::fail(KV_EINVAL, "tier: block table or chunk ids do not match n_tokens");
-        if (h.n_tokens == 0)
-            return KV_OK;
-        kv_status vst = kvx::check_layout(lay);
-        if (vst != KV_OK)
-            return vst;
+        kv_status st = kvx::check_layout(lay);
+        if (st != KV_OK)
+            return st;
         if (h.block_stride_bytes < 0)
             return kvx::fail(KV_EINVAL, "tier: negative block stride");
         const kvx::Geometry g = kvx::geometry(lay, h.block_stride_bytes);
-
-        // Map the replica's layers (each allocation once per connection).
         layers_.resize(static_cast<size_t>(h.num_layers));
         for (int32_t l = 0; l < h.num_layers; ++l) {
             std::array<uint8_t, 64> key;
@@ -211,27 +219,29 @@ class Connection {
             KVX_HIP(hipHostMalloc(reinterpret_cast<void **>(&table_pinned_), table_bytes, hipHostMallocDefault));
             table_cap_ = table_bytes;
         }
-        std::memcpy(table_pinned_, table_host_.data(), table_bytes);
-        KVX_HIP(hipMemcpyAsync(table_, table_pinned_, table_bytes, hipMemcpyHostToDevice, stream_));
+        if (table_bytes) {
+            std::memcpy(table_pinned_, table_host_.data(), table_bytes);
+            KVX_HIP(hipMemcpyAsync(table_, table_pinned_, table_bytes, hipMemcpyHostToDevice, stream_));
+        }
 
-        kv_cache cache;
-        std::memset(&cache, 0, sizeof(cache));
-        cache.layout = lay;
-        cache.num_blocks = h.num_blocks;
-        cache.device = pool_->device;
-        cache.block_order = h.block_order;
-        cache.layer_ptrs = layers_.data();
-        cache.block_stride_bytes = h.block_stride_bytes;
+        std::memset(cache, 0, sizeof(*cache));
+        cache->layout = lay;
+        cache->num_blocks = h.num_blocks;
+        cache->device = pool_->device;
+        cache->block_order = h.block_order;
+        cache->layer_ptrs = layers_.data();
+        cache->block_stride_bytes = h.block_stride_bytes;
+        return KV_OK;
+    }
 
-        (void)kv_pool_async_error(pool_, 1);
-        kv_status st = h.op == kOpStore ? kv_store(&cache, table_, h.n_tokens, pool_, ids_.data(), stream_)
-                                        : kv_load(&cache, table_, h.n_tokens, pool_, ids_.data(), stream_);
-        const std::string enqueue_error = st != KV_OK ? std::string(kv_last_error()) : std::string();
-        // Complete whatever was enqueued before replying (the host-side completion).
+    // Complete everything enqueued on this connection's stream; then the request's own status
+    // (an enqueue error, a failed synchronisation or a device-side fault, in that order).
+    kv_status complete(kv_status enqueued) {
+        const std::string enqueue_error = enqueued != KV_OK ? std::string(kv_last_error()) : std::string();
         const hipError_t e = hipStreamSynchronize(stream_);
-        if (st != KV_OK) {
+        if (enqueued != KV_OK) {
             kvx::set_last_error(enqueue_error);
-            return st;
+            return enqueued;
         }
         if (e != hipSuccess)
             return kvx::hip_fail(e, "hipStreamSynchronize(tier)", __FILE__, __LINE__);
@@ -242,7 +252,98 @@ class Connection {
         return KV_OK;
     }
 
+    kv_status execute(const RequestHeader &h, int64_t *value) {
+        const kv_layout &lay = h.layout;
+        if (lay.block_size < 1 || lay.chunk_tokens < 1 || h.n_tokens < 0 || lay.num_layers != h.num_layers)
+            return kvx::fail(KV_EINVAL, "tier: request layout or length is invalid");
+        if (h.n_table != ceil_div(h.n_tokens, lay.block_size))
+            return kvx::fail(KV_EINVAL, "tier: block table does not match n_tokens");
+        const bool prefix = h.op == kOpStorePrefix || h.op == kOpLoadPrefix;
+        if (!prefix && (h.n_chunks != ceil_div(h.n_tokens, lay.chunk_tokens) || h.n_ids != 0))
+            return kvx::fail(KV_EINVAL, "tier: chunk ids do not match n_tokens");
+        if (prefix && (h.n_ids != h.n_tokens || h.n_chunks != 0))
+            return kvx::fail(KV_EINVAL, "tier: a prefix request carries its n_tokens token ids and no chunk ids");
+        if (prefix && !index_)
+            return kvx::fail(KV_EINVAL, "tier: this tier serves no index, so it takes no prefix requests");
+        if (prefix && (kvx::index_chunk_tokens(index_) != lay.chunk_tokens ||
+                       kvx::index_num_slots(index_) > pool_->num_slots))
+            return kvx::fail(KV_EINVAL, "tier: the index does not match the pool (chunk length or slot count)");
+        if (h.n_tokens == 0)
+            return KV_OK;
+
+        kv_cache cache;
+        kv_status st = map_cache(h, &cache);
+        if (st != KV_OK)
+            return complete(st);
+        (void)kv_pool_async_error(pool_, 1);
+        switch (h.op) {
+        case kOpStore:
+            return complete(kv_store(&cache, table_, h.n_tokens, pool_, ids_.data(), stream_));
+        case kOpLoad:
+            return complete(kv_load(&cache, table_, h.n_tokens, pool_, ids_.data(), stream_));
+        case kOpStorePrefix:
+            return store_prefix(h, cache, value);
+        default:
+            return load_prefix(h, cache, value);
+        }
+    }
+
+    kv_status store_prefix(const RequestHeader &h, const kv_cache &cache, int64_t *stored) {
+        const int64_t C = h.layout.chunk_tokens, bpc = C / h.layout.block_size;
+        const int64_t nfull = h.n_tokens / C;
+        slots_.resize(static_cast<size_t>(nfull));
+        is_new_.resize(static_cast<size_t>(nfull));
+        int64_t n_chunks = 0;
+        kv_status st = kv_index_reserve(index_, h.salt, tokens_.data(), h.n_tokens, slots_.data(), is_new_.data(),
+                                        &n_chunks);
+        if (st != KV_OK)
+            return complete(st);
+        // Runs of consecutive new chunks, one store each (chunk i uses table entries from i*C/BS).
+        int64_t count = 0;
+        for (int64_t a = 0; a < n_chunks && st == KV_OK;) {
+            if (!is_new_[a]) {
+                ++a;
+                continue;
+            }
+            int64_t b = a;
+            while (b < n_chunks && is_new_[b])
+                ++b;
+            st = kv_store(&cache, table_ + a * bpc, (b - a) * C, pool_, slots_.data() + a, stream_);
+            if (st == KV_OK)
+                count += b - a;
+            a = b;
+        }
+        st = complete(st);
+        // Publish only chunks whose stores completed without fault (Sec. 3.2); else abort them all.
+        const kv_status commit = kv_index_commit(index_, slots_.data(), is_new_.data(), n_chunks, st == KV_OK);
+        if (st != KV_OK)
+            return st;
+        if (commit != KV_OK)
+            return commit;
+        *stored = count;
+        return KV_OK;
+    }
+
+    kv_status load_prefix(const RequestHeader &h, const kv_cache &cache, int64_t *hit_tokens) {
+        const int64_t nfull = h.n_tokens / h.layout.chunk_tokens;
+        slots_.resize(static_cast<size_t>(nfull));
+        kv_lookup hit;
+        kv_status st = kv_index_lookup(index_, h.salt, tokens_.data(), h.n_tokens, KV_LOOKUP_PIN, slots_.data(), &hit);
+        if (st != KV_OK)
+            return complete(st);
+        st = hit.hit_tokens ? kv_load(&cache, table_, hit.hit_tokens, pool_, slots_.data(), stream_) : KV_OK;
+        st = complete(st);
+        const kv_status unpin = kv_index_unpin(index_, slots_.data(), hit.hit_chunks);
+        if (st != KV_OK)
+            return st;
+        if (unpin != KV_OK)
+            return unpin;
+        *hit_tokens = hit.hit_tokens;
+        return KV_OK;
+    }
+
     kv_pool *pool_;
+    kv_index *index_;
     int fd_;
     hipStream_t stream_ = nullptr;
     int32_t *table_ = nullptr;
@@ -256,11 +357,15 @@ class Connection {
     std::vector<kv_ipc_buffer> bufs_;
     std::vector<int32_t> table_host_;
     std::vector<int64_t> ids_;
+    std::vector<int32_t> tokens_;
+    std::vector<int64_t> slots_;
+    std::vector<uint8_t> is_new_;
     std::vector<void *> layers_;
 };
 
-kv_status tier_request(uint32_t op, int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
-                       const int64_t *chunk_ids, void *stream) {
+kv_status send_request(uint32_t op, int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
+                       const int64_t *chunk_ids, uint64_t salt, const int32_t *tokens, void *stream,
+                       int64_t *value) {
     if (!cache)
         return kvx::fail(KV_EINVAL, "cache must not be NULL");
     kv_status st = kvx::check_layout(cache->layout);
@@ -268,10 +373,12 @@ kv_status tier_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
         return st;
     if (n_tokens < 0)
         return kvx::fail(KV_EINVAL, "n_tokens must be >= 0 (got %lld)", static_cast<long long>(n_tokens));
+    const bool prefix = op == kOpStorePrefix || op == kOpLoadPrefix;
     if (n_tokens == 0)
         return KV_OK;
-    if (!block_table || !chunk_ids || !cache->layer_ptrs)
-        return kvx::fail(KV_EINVAL, "block_table, chunk_ids and layer_ptrs must not be NULL for n_tokens > 0");
+    if (!block_table || !cache->layer_ptrs || (prefix ? !tokens : !chunk_ids))
+        return kvx::fail(KV_EINVAL, "block_table, layer_ptrs and %s must not be NULL for n_tokens > 0",
+                         prefix ? "tokens" : "chunk_ids");
     const int32_t L = cache->layout.num_layers;
     if (L > kMaxLayers)
         return kvx::fail(KV_EUNSUPPORTED, "more than %d layers", kMaxLayers);
@@ -290,7 +397,9 @@ kv_status tier_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
     h.block_stride_bytes = cache->block_stride_bytes;
     h.n_tokens = n_tokens;
     h.n_table = ceil_div(n_tokens, cache->layout.block_size);
-    h.n_chunks = ceil_div(n_tokens, cache->layout.chunk_tokens);
+    h.n_chunks = prefix ? 0 : ceil_div(n_tokens, cache->layout.chunk_tokens);
+    h.n_ids = prefix ? n_tokens : 0;
+    h.salt = salt;
     std::vector<kv_ipc_buffer> bufs(static_cast<size_t>(L));
     for (int32_t l = 0; l < L; ++l) {
         st = kv_ipc_export(cache->layer_ptrs[l], &bufs[static_cast<size_t>(l)]);
@@ -299,7 +408,8 @@ kv_status tier_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
     }
     if (!write_full(fd, &h, sizeof(h)) || !write_full(fd, bufs.data(), bufs.size() * sizeof(kv_ipc_buffer)) ||
         !write_full(fd, block_table, static_cast<size_t>(h.n_table) * sizeof(int32_t)) ||
-        !write_full(fd, chunk_ids, static_cast<size_t>(h.n_chunks) * sizeof(int64_t)))
+        (h.n_chunks && !write_full(fd, chunk_ids, static_cast<size_t>(h.n_chunks) * sizeof(int64_t))) ||
+        (h.n_ids && !write_full(fd, tokens, static_cast<size_t>(h.n_ids) * sizeof(int32_t))))
         return kvx::fail(KV_EINVAL, "tier connection failed while sending (%s)", std::strerror(errno));
     ReplyHeader r;
     if (!read_full(fd, &r, sizeof(r)) || r.magic != kMagic || r.msg_len > (1u << 20))
@@ -307,9 +417,13 @@ kv_status tier_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
     std::string msg(r.msg_len, '\0');
     if (r.msg_len && !read_full(fd, &msg[0], r.msg_len))
         return kvx::fail(KV_EINVAL, "tier connection failed while reading the reply");
-    if (r.status != KV_OK)
+    if (r.status != KV_OK) {
         kvx::set_last_error("tier: " + msg);
-    return r.status;
+        return r.status;
+    }
+    if (value)
+        *value = r.value;
+    return KV_OK;
 }
 
 }  // namespace
@@ -336,21 +450,104 @@ kv_status kv_ipc_export(const void *dev_ptr, kv_ipc_buffer *out) {
     return KV_OK;
 }
 
-kv_status kv_tier_serve(kv_pool *pool, int fd) {
+kv_status kv_tier_serve(kv_pool *pool, kv_index *index, int fd) {
     if (!pool || fd < 0)
         return kvx::fail(KV_EINVAL, "pool must not be NULL and fd must be a connected socket");
-    Connection c(pool, fd);
+    Connection c(pool, index, fd);
     return c.serve();
+}
+
+kv_status kv_tier_listen(const char *path, int *listen_fd) {
+    if (!path || !listen_fd)
+        return kvx::fail(KV_EINVAL, "path and listen_fd must not be NULL");
+    sockaddr_un addr;
+    std::memset(&addr, 0, sizeof(addr));
+    addr.sun_family = AF_UNIX;
+    if (std::strlen(path) >= sizeof(addr.sun_path))
+        return kvx::fail(KV_EINVAL, "socket path longer than %zu bytes", sizeof(addr.sun_path) - 1);
+    std::strncpy(addr.sun_path, path, sizeof(addr.sun_path) - 1);
+    const int fd = socket(AF_UNIX, SOCK_STREAM, 0);
+    if (fd < 0)
+        return kvx::fail(KV_EINVAL, "socket: %s", std::strerror(errno));
+    if (bind(fd, reinterpret_cast<sockaddr *>(&addr), sizeof(addr)) != 0 || listen(fd, 64) != 0) {
+        const int err = errno;
+        close(fd);
+        return kvx::fail(KV_EINVAL, "cannot listen at %s: %s", path, std::strerror(err));
+    }
+    *listen_fd = fd;
+    return KV_OK;
+}
+
+kv_status kv_tier_run(kv_pool *pool, kv_index *index, int listen_fd, int32_t connections) {
+    if (!pool || listen_fd < 0 || connections < 0)
+        return kvx::fail(KV_EINVAL, "pool must not be NULL, listen_fd a listening socket, connections >= 0");
+    struct Result {
+        kv_status status = KV_OK;
+        std::string message;
+    };
+    std::deque<Result> results;  // push_back keeps references to earlier elements valid
+    std::vector<std::thread> threads;
+    kv_status accept_error = KV_OK;
+    std::string accept_message;
+    for (int32_t k = 0; connections == 0 || k < connections;) {
+        const int fd = accept(listen_fd, nullptr, nullptr);
+        if (fd < 0) {
+            if (errno == EINTR)
+                continue;
+            accept_error = KV_EINVAL;
+            accept_message = std::string("accept: ") + std::strerror(errno);
+            break;
+        }
+        ++k;
+        results.emplace_back();
+        Result *r = &results.back();
+        threads.emplace_back([pool, index, fd, r] {
+            r->status = kv_tier_serve(pool, index, fd);
+            if (r->status != KV_OK)
+                r->message = kv_last_error();
+            close(fd);
+        });
+    }
+    for (std::thread &t : threads)
+        t.join();
+    for (const Result &r : results)
+        if (r.status != KV_OK) {
+            kvx::set_last_error(r.message);
+            return r.status;
+        }
+    if (accept_error != KV_OK)
+        return kvx::fail(accept_error, "%s", accept_message.c_str());
+    return KV_OK;
 }
 
 kv_status kv_tier_store(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                         const int64_t *chunk_ids, void *stream) {
-    return tier_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, stream);
+    return send_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, stream, nullptr);
 }
 
 kv_status kv_tier_load(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                        const int64_t *chunk_ids, void *stream) {
-    return tier_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, stream);
+    return send_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, stream, nullptr);
+}
+
+kv_status kv_tier_store_prefix(int fd, const kv_cache *cache, const int32_t *block_table, uint64_t salt,
+                               const int32_t *tokens, int64_t n_tokens, int64_t *stored_chunks, void *stream) {
+    int64_t v = 0;
+    const kv_status st =
+        send_request(kOpStorePrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, stream, &v);
+    if (stored_chunks)
+        *stored_chunks = st == KV_OK ? v : 0;
+    return st;
+}
+
+kv_status kv_tier_load_prefix(int fd, const kv_cache *cache, const int32_t *block_table, uint64_t salt,
+                              const int32_t *tokens, int64_t n_tokens, int64_t *hit_tokens, void *stream) {
+    int64_t v = 0;
+    const kv_status st =
+        send_request(kOpLoadPrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, stream, &v);
+    if (hit_tokens)
+        *hit_tokens = st == KV_OK ? v : 0;
+    return st;
 }
 
 }  // extern "C"

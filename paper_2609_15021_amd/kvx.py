@@ -131,7 +131,13 @@ def _open():
         "kv_index_commit_state": ([P, i64, ctypes.c_int], i32),
         "kv_index_get_stats": ([P, ctypes.POINTER(KvIndexStats)], i32),
         "kv_ipc_export": ([P, ctypes.POINTER(KvIpcBuffer)], i32),
-        "kv_tier_serve": ([P, ctypes.c_int], i32),
+        "kv_tier_serve": ([P, P, ctypes.c_int], i32),
+        "kv_tier_listen": ([ctypes.c_char_p, ctypes.POINTER(ctypes.c_int)], i32),
+        "kv_tier_run": ([P, P, ctypes.c_int, i32], i32),
+        "kv_tier_store_prefix": ([ctypes.c_int, ctypes.POINTER(KvCache), P, ctypes.c_uint64, P, i64,
+                                  ctypes.POINTER(i64), P], i32),
+        "kv_tier_load_prefix": ([ctypes.c_int, ctypes.POINTER(KvCache), P, ctypes.c_uint64, P, i64,
+                                 ctypes.POINTER(i64), P], i32),
         "kv_tier_store": ([ctypes.c_int, ctypes.POINTER(KvCache), P, i64, P, P], i32),
         "kv_tier_load": ([ctypes.c_int, ctypes.POINTER(KvCache), P, i64, P, P], i32),
         "kv_last_error": ([], ctypes.c_char_p),
@@ -153,7 +159,8 @@ EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slo
            "kv_check_state", "kv_store_state", "kv_load_state", "kv_index_create", "kv_index_destroy",
            "kv_index_keys", "kv_index_lookup", "kv_index_unpin", "kv_index_reserve", "kv_index_commit",
            "kv_index_reserve_state", "kv_index_commit_state", "kv_index_get_stats", "kv_ipc_export",
-           "kv_tier_serve", "kv_tier_store", "kv_tier_load")
+           "kv_tier_serve", "kv_tier_store", "kv_tier_load", "kv_tier_listen", "kv_tier_run",
+           "kv_tier_store_prefix", "kv_tier_load_prefix")
 
 
 def kv_last_error() -> str:
@@ -515,10 +522,24 @@ def kv_ipc_export(ptr) -> KvIpcBuffer:
     return out
 
 
-def kv_tier_serve(pool: Pool, fd: int) -> None:
+def kv_tier_serve(pool: Pool, fd: int, index: Index = None) -> None:
     """Serve one replica connection on the connected stream socket ``fd`` until it closes (blocks;
-    the GIL is released while it runs)."""
-    _raise(_lib.kv_tier_serve(pool.handle, int(fd)))
+    the GIL is released while it runs); ``index`` enables prefix requests."""
+    _raise(_lib.kv_tier_serve(pool.handle, index.handle if index is not None else None, int(fd)))
+
+
+def kv_tier_listen(path: str) -> int:
+    """A listening stream socket at ``path`` (which must not exist); returns its fd."""
+    fd = ctypes.c_int(-1)
+    _raise(_lib.kv_tier_listen(os.fsencode(path), ctypes.byref(fd)))
+    return fd.value
+
+
+def kv_tier_run(pool: Pool, listen_fd: int, connections: int, index: Index = None) -> None:
+    """Accept and serve ``connections`` replica connections (0 = until the socket fails), each on
+    its own native thread; returns when all have ended."""
+    _raise(_lib.kv_tier_run(pool.handle, index.handle if index is not None else None, int(listen_fd),
+                            int(connections)))
 
 
 def _host_table(block_table):
@@ -539,3 +560,23 @@ def kv_tier_load(fd: int, cache: Cache, block_table, n_tokens: int, chunk_ids, s
     t, tp = _host_table(block_table)
     ids, ip = _chunk_ids(chunk_ids)
     _raise(_lib.kv_tier_load(int(fd), ctypes.byref(cache.struct), tp, int(n_tokens), ip, _stream_handle(stream)))
+
+
+def kv_tier_store_prefix(fd: int, cache: Cache, block_table, salt: int, tokens, stream=None) -> int:
+    """Store the prompt's whole chunks that the tier does not hold yet; returns the chunks stored."""
+    t, tp = _host_table(block_table)
+    tok, kp = _tokens(tokens)
+    out = ctypes.c_int64()
+    _raise(_lib.kv_tier_store_prefix(int(fd), ctypes.byref(cache.struct), tp, int(salt) & 0xFFFFFFFFFFFFFFFF, kp,
+                                     int(tok.size), ctypes.byref(out), _stream_handle(stream)))
+    return int(out.value)
+
+
+def kv_tier_load_prefix(fd: int, cache: Cache, block_table, salt: int, tokens, stream=None) -> int:
+    """Load the prompt's longest whole-chunk hit into the cache; returns the hit tokens."""
+    t, tp = _host_table(block_table)
+    tok, kp = _tokens(tokens)
+    out = ctypes.c_int64()
+    _raise(_lib.kv_tier_load_prefix(int(fd), ctypes.byref(cache.struct), tp, int(salt) & 0xFFFFFFFFFFFFFFFF, kp,
+                                    int(tok.size), ctypes.byref(out), _stream_handle(stream)))
+    return int(out.value)

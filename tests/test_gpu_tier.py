@@ -29,9 +29,9 @@ def _dims(lay):
     return [str(v) for v in (lay.L, lay.H, lay.D, lay.E, lay.BS, lay.C)]
 
 
-def _start_tier(sock, lay, slots, mode, nconn, dump):
-    p = subprocess.Popen([sys.executable, "-u", ROLES, "tier", sock, *_dims(lay), str(slots), mode, str(nconn), dump],
-                         stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+def _start_tier(sock, lay, slots, mode, nconn, dump, role="tier", extra=()):
+    p = subprocess.Popen([sys.executable, "-u", ROLES, role, sock, *_dims(lay), str(slots), mode, str(nconn), dump,
+                          *extra], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     t0 = time.time()
     while time.time() - t0 < 90:
         line = p.stdout.readline()
@@ -153,10 +153,8 @@ def test_tier_survives_a_malformed_connection(tmp_path):
     n = 512
     nc, NB = lay.nc(n), 64
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
-    p = subprocess.Popen([sys.executable, "-u", ROLES, "tier", sock, *_dims(lay), str(nc), "staged", "2", dump],
-                         stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    p = _start_tier(sock, lay, nc, "staged", 2, dump)
     try:
-        assert p.stdout.readline().startswith("READY")
         bad = _connect(sock)
         bad.sendall(b"\x00" * 160)  # a full header's worth of bytes with the wrong magic
         bad.close()
@@ -173,3 +171,89 @@ def test_tier_survives_a_malformed_connection(tmp_path):
     results = [ln for ln in out.splitlines() if ln.startswith("TIER")][-1].split(" ", 1)[1].split(";")
     assert sorted(r == "ok" for r in results) == [False, True], results
     assert any("malformed" in r for r in results), results
+
+
+def _start_native_tier(sock, lay, slots, mode, nconn, dump, index_slots):
+    return _start_tier(sock, lay, slots, mode, nconn, dump, role="tier-native", extra=(str(index_slots),))
+
+
+def _finish_native(p):
+    out, _ = p.communicate(timeout=90)
+    assert p.returncode == 0, out[-2000:]
+    assert [ln for ln in out.splitlines() if ln.startswith("TIER")][-1] == "TIER ok", out[-2000:]
+    return out
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_prefix_store_and_external_hit(mode, tmp_path):
+    """The tier as a prefix cache (library listener and threads, pool index): replica A stores a
+    prompt; replica B asks for the same prompt and gets its whole chunks as an external hit
+    (Sec. 3.1-3.2: hits are whole chunks), loaded bit-exactly; a prompt that diverges inside chunk
+    3 hits 3 chunks; a new salt hits nothing; storing the prompt again writes nothing new."""
+    lay = TINY
+    n = 5 * lay.C + 100                      # 5 whole chunks and a partial one (not kept)
+    NB = lay.nblk(n) + 9
+    seed, salt = harness.sub_seed("prefix", mode), 11
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    tier = _start_native_tier(sock, lay, 8, mode, 3, dump, 8)
+    try:
+        r = subprocess.run([sys.executable, "-u", ROLES, "store-prefix", sock, *_dims(lay), str(NB), str(n), str(seed),
+                            str(salt)], capture_output=True, text=True, timeout=120)
+        assert r.returncode == 0 and "STORED 5" in r.stdout, (r.stdout + r.stderr)[-3000:]
+        tokens = harness.prompt_tokens(seed, n)
+        btB = harness.block_table(seed + 2, NB, lay.nblk(n))
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
+        cB = kvx.Cache(dB, lay.kv, NB)
+        torch.cuda.synchronize()
+        c = _connect(sock)
+        hit = kvx.kv_tier_load_prefix(c.fileno(), cB, btB, salt, tokens)
+        got_B = dB.cpu()
+        other = tokens.copy()
+        other[3 * lay.C + 7] ^= 1
+        assert kvx.kv_tier_load_prefix(c.fileno(), cB, btB, salt, other) == 3 * lay.C
+        assert kvx.kv_tier_load_prefix(c.fileno(), cB, btB, salt + 1, tokens) == 0
+        c.close()
+        c2 = _connect(sock)                  # a third replica re-stores the same prompt: nothing new
+        dC = torch.zeros_like(dB)
+        torch.cuda.synchronize()
+        assert kvx.kv_tier_store_prefix(c2.fileno(), kvx.Cache(dC, lay.kv, NB), btB, salt, tokens) == 0
+        c2.close()
+    finally:
+        out = _finish_native(tier)
+    assert hit == 5 * lay.C
+    A = host_cache(lay, NB, seed, "raw")
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+    pool = np.load(dump)
+    # The index gave chunks 0..4 slots 0..4 (lowest free first); slots 5..7 were never written.
+    want_pool = oracle_pool(lay, A, btA, hit, np.arange(5), 8, POOL_SENT)
+    assert np.array_equal(pool, want_pool), first_mismatch(pool, want_pool)
+    want_B = oracle_unpack_into(lay, np.zeros_like(A), btB, hit, want_pool, np.arange(5))
+    got = got_B.numpy().view(A.dtype).reshape(A.shape)
+    assert np.array_equal(got, want_B), first_mismatch(got, want_B)
+    assert "'entries': 5" in out and "'evictions': 0" in out
+
+
+def test_prefix_eviction_under_a_small_pool(tmp_path):
+    """With 4 slots, storing a 3-chunk prompt and then a 3-chunk different prompt evicts the first
+    prompt's tail (LRU, tails first): the first prompt then hits 1 chunk, the second all 3."""
+    lay = TINY
+    n = 3 * lay.C
+    NB = lay.nblk(n) + 4
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    tier = _start_native_tier(sock, lay, 4, "staged", 3, dump, 4)
+    try:
+        for seed in (101, 202):
+            r = subprocess.run([sys.executable, "-u", ROLES, "store-prefix", sock, *_dims(lay), str(NB), str(n),
+                                str(seed), "5"], capture_output=True, text=True, timeout=120)
+            assert r.returncode == 0 and "STORED 3" in r.stdout, (r.stdout + r.stderr)[-3000:]
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
+        cB = kvx.Cache(dB, lay.kv, NB)
+        bt = np.arange(lay.nblk(n), dtype=np.int32)
+        torch.cuda.synchronize()
+        c = _connect(sock)
+        assert kvx.kv_tier_load_prefix(c.fileno(), cB, bt, 5, harness.prompt_tokens(101, n)) == 1 * lay.C
+        assert kvx.kv_tier_load_prefix(c.fileno(), cB, bt, 5, harness.prompt_tokens(202, n)) == 3 * lay.C
+        c.close()
+    finally:
+        out = _finish_native(tier)
+    assert "'evictions': 2" in out

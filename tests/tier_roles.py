@@ -1,10 +1,15 @@
 """Process roles for the tier tests (run as separate processes by tests/test_gpu_tier.py).
 
-  tier  SOCK L H D E BS C SLOTS MODE NCONN DUMP   own the pool, serve NCONN replica connections,
-                                                  then save the pool bytes to DUMP
+  tier  SOCK L H D E BS C SLOTS MODE NCONN DUMP   own the pool, serve NCONN replica connections
+                                                  (one Python thread each), then save the pool bytes
+                                                  to DUMP
+  tier-native  (same arguments) INDEX_SLOTS        the same with the library's own listener and threads,
+                                                  and a pool index over INDEX_SLOTS slots
   store SOCK L H D E BS C NB N SEED DELAY_MS      replica A: its cache from the seeded generator
                                                   (DELAY_MS > 0: zeros, then a delayed producer
                                                   writes byte 37 on its stream), stored through the tier
+  store-prefix SOCK L H D E BS C NB N SEED SALT    replica A stores the prompt harness.prompt_tokens(SEED, N)
+                                                  by prefix; prints the chunks it stored
 """
 import os
 import socket
@@ -58,6 +63,45 @@ def tier(sock, L, H, D, E, BS, C, slots, mode, nconn, dump):
     kvx.kv_pool_destroy(pool)
 
 
+def tier_native(sock, L, H, D, E, BS, C, slots, mode, nconn, dump, index_slots):
+    lay = kvx.make_layout(L, H, D, E, BS, C)
+    pool = kvx.kv_pool_create(lay, slots, mode, staging_slots=2, chunks_per_batch=2)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    index = kvx.kv_index_create(C, index_slots) if index_slots else None
+    fd = kvx.kv_tier_listen(sock)
+    print("READY", flush=True)
+    try:
+        kvx.kv_tier_run(pool, fd, nconn, index)
+        result = "ok"
+    except kvx.KvError as e:
+        result = repr(e)
+    os.close(fd)
+    np.save(dump, view.copy())
+    if index is not None:
+        print("INDEX", kvx.kv_index_get_stats(index), flush=True)
+    print("TIER", result, flush=True)
+    kvx.kv_pool_destroy(pool)
+
+
+def replica_cache(L, H, D, E, BS, C, NB, seed):
+    lay = kvx.make_layout(L, H, D, E, BS, C)
+    A = harness.gen_cache(seed, "raw", L, NB, H, BS, D, E)
+    dA = torch.from_numpy(A.view({1: np.uint8, 2: np.int16, 4: np.int32}[E])).to("cuda:0")
+    torch.cuda.synchronize()
+    return dA, kvx.Cache(dA, lay, NB)
+
+
+def store_prefix(sock, L, H, D, E, BS, C, NB, n, seed, salt):
+    dA, cache = replica_cache(L, H, D, E, BS, C, NB, seed)
+    bt = harness.block_table(seed + 1, NB, -(-n // BS))
+    c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    c.connect(sock)
+    stored = kvx.kv_tier_store_prefix(c.fileno(), cache, bt, salt, harness.prompt_tokens(seed, n))
+    c.close()
+    print("STORED", stored, flush=True)
+
+
 def store(sock, L, H, D, E, BS, C, NB, n, seed, delay_ms):
     lay = kvx.make_layout(L, H, D, E, BS, C)
     A = harness.gen_cache(seed, "raw", L, NB, H, BS, D, E)
@@ -82,7 +126,11 @@ if __name__ == "__main__":
     role, args = sys.argv[1], sys.argv[2:]
     if role == "tier":
         tier(args[0], *map(int, args[1:8]), args[8], int(args[9]), args[10])
+    elif role == "tier-native":
+        tier_native(args[0], *map(int, args[1:8]), args[8], int(args[9]), args[10], int(args[11]))
     elif role == "store":
         store(args[0], *map(int, args[1:12]))
+    elif role == "store-prefix":
+        store_prefix(args[0], *map(int, args[1:12]))
     else:
         raise SystemExit(f"unknown role {role}")

@@ -372,39 +372,26 @@ def layer_caches(torch, hg, kvx, nb, dev, seed=None):
 
 
 def tier_server(torch, kvx, sock, mode):
-    import socket
-    import threading
+    """The tier process: the pool, a pool index over its slots, the library's own listener."""
     pool = kvx.kv_pool_create(kvx.make_layout(L, H, D, E, BS, C), -(-TIER_N // C), mode, profile=True)
-    srv = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
-    srv.bind(sock)
-    srv.listen(4)
-    srv.settimeout(300)
+    index = kvx.kv_index_create(C, -(-TIER_N // C))
+    fd = kvx.kv_tier_listen(sock)
     print("READY", flush=True)
     errors = []
-
-    def serve(conn):
-        try:
-            kvx.kv_tier_serve(pool, conn.fileno())
-        except Exception as e:  # reported through stdout
-            errors.append(repr(e))
-        finally:
-            conn.close()
-
-    threads = []
-    for _ in range(2):  # replica A, then replica B
-        conn, _ = srv.accept()
-        threads.append(threading.Thread(target=serve, args=(conn,)))
-        threads[-1].start()
-    for t in threads:
-        t.join()
+    try:
+        kvx.kv_tier_run(pool, fd, 2, index)  # replica A, then replica B
+    except kvx.KvError as e:
+        errors.append(repr(e))
+    os.close(fd)
     kern = {}
     for w in ("pack", "unpack"):
         n, ms, alg = kvx.kv_pool_kernel_stats(pool, w)
         if n:
             kern[w] = {"launches": n, "avg_launch_ms": round(ms / n, 4),
                        "achieved_GBps": round(alg / (ms / 1e3) / 1e9, 1)}
+    stats = kvx.kv_index_get_stats(index)
     kvx.kv_pool_destroy(pool)
-    print(json.dumps({"errors": errors, "kernels": kern}), flush=True)
+    print(json.dumps({"errors": errors, "kernels": kern, "index": stats}), flush=True)
     sys.exit(1 if errors else 0)
 
 
@@ -416,15 +403,16 @@ def tier_store(np, torch, harness, hg, kvx, sock, dev):
     c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
     c.connect(sock)
     t0 = time.perf_counter()
-    kvx.kv_tier_store(c.fileno(), cache, bt, TIER_N, np.arange(TIER_N // C))
+    stored = kvx.kv_tier_store_prefix(c.fileno(), cache, bt, 1, harness.prompt_tokens(seed, TIER_N))
     dt = time.perf_counter() - t0
     c.close()
-    print(json.dumps({"store_s": dt}), flush=True)
+    print(json.dumps({"store_s": dt, "stored_chunks": stored}), flush=True)
 
 
 def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
-    """Replica A (a process) stores a 128k prefix through a tier process that owns the pool;
-    replica B (this process) restores it: host wall clock of each request, handshake included."""
+    """Replica A (a process) stores a 128k-token prompt by prefix through a tier process that owns
+    the pool and its index; replica B (this process) asks for the same prompt and restores its
+    external hit: host wall clock of each request, keying and handshake included."""
     import socket
     import subprocess
     import tempfile
@@ -441,23 +429,26 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
                            timeout=300)
         if r.returncode != 0:
             raise RuntimeError("replica A failed: " + r.stderr[-2000:])
-        store_s = json.loads(r.stdout.strip().splitlines()[-1])["store_s"]
+        a_out = json.loads(r.stdout.strip().splitlines()[-1])
+        store_s = a_out["store_s"]
         seed = harness.sub_seed("bench-tier", TIER_N)
         layers_b, cache_b = layer_caches(torch, hg, kvx, TIER_NB, dev)
         bt_a = harness.block_table(seed + 1, TIER_NB, TIER_N // BS)
         bt_b = harness.block_table(seed + 2, TIER_NB, TIER_N // BS)
         c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
         c.connect(sock)
-        restore = []
+        restore, hits = [], []
+        prompt = harness.prompt_tokens(seed, TIER_N)
         for _ in range(reps):
             t0 = time.perf_counter()
-            kvx.kv_tier_load(c.fileno(), cache_b, bt_b, TIER_N, np.arange(TIER_N // C))
+            hits.append(kvx.kv_tier_load_prefix(c.fileno(), cache_b, bt_b, 1, prompt))
             restore.append(time.perf_counter() - t0)
         c.close()
         out, err = tier.communicate(timeout=120)
         if tier.returncode != 0:
             raise RuntimeError("tier failed: " + (out + err)[-2000:])
-        kern = json.loads(out.strip().splitlines()[-1])["kernels"]
+        tier_out = json.loads(out.strip().splitlines()[-1])
+        kern = tier_out["kernels"]
     finally:
         if tier.poll() is None:
             tier.kill()
@@ -473,14 +464,18 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
     nc = TIER_N // C
     ok, msg = sampled_round_trip(np, harness, stacked, bt_a, bt_b, seed, TIER_N, TIER_NB, [0, nc // 2, nc - 1],
                                  torch)
+    ok = ok and a_out["stored_chunks"] == nc and all(h == TIER_N for h in hits)
     N = TIER_N * TOKEN_BYTES
-    return {"workload": "replica A (a process) stores the 131,072-token 27B-class prefix through a tier process "
-                        "that owns the pinned pool; replica B (another process) restores it; caches shared by HIP "
-                        "IPC, one allocation per layer; host-side completion at both ends",
-            "mode": mode, "store_s": round(store_s, 4), "store_GBps": round(N / store_s / 1e9, 3),
+    return {"workload": "replica A (a process) stores a 131,072-token prompt of the 27B-class layout by prefix "
+                        "through a tier process that owns the pinned pool and its index; replica B (another "
+                        "process) asks for the same prompt and restores its external hit; caches shared by HIP IPC, "
+                        "one allocation per layer; host-side completion at both ends",
+            "mode": mode, "stored_chunks": a_out["stored_chunks"], "external_hit_tokens": hits[0],
+            "store_s": round(store_s, 4), "store_GBps": round(N / store_s / 1e9, 3),
             "restore_s_first": round(restore[0], 4), "restore_s": round(statistics.median(restore[1:] or restore), 4),
             "restore_GBps": round(N / statistics.median(restore[1:] or restore) / 1e9, 3),
-            "tier_kernels": kern, "round_trip": msg if ok else f"FAILED: {msg}"}, ok
+            "tier_kernels": kern, "tier_index": tier_out["index"],
+            "round_trip": msg if ok else f"FAILED: {msg}"}, ok
 
 
 def cpu_baseline(np, oracle, n_chunks=64):
@@ -586,7 +581,7 @@ def main():
         tier, tier_ok = child_leg("--tier-only")
         if "error" not in tier:
             for m, t in tier.items():
-                log(f"[bench] tier ({m}, 3 processes): store {t['store_s']} s ({t['store_GBps']} GB/s), restore "
+                log(f"[bench] tier ({m}, 3 processes): {t['external_hit_tokens']} tokens hit; store {t['store_s']} s ({t['store_GBps']} GB/s), restore "
                     f"{t['restore_s']} s ({t['restore_GBps']} GB/s, first {t['restore_s_first']} s); "
                     f"{t['round_trip']}")
     paper_ok = paper_ok and state_ok and tier_ok

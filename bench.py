@@ -403,7 +403,7 @@ def tier_store(np, torch, harness, hg, kvx, sock, dev):
     c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
     c.connect(sock)
     t0 = time.perf_counter()
-    stored = kvx.kv_tier_store_prefix(c.fileno(), cache, bt, 1, harness.prompt_tokens(seed, TIER_N))
+    stored, _ = kvx.kv_tier_store_prefix(c.fileno(), cache, bt, 1, harness.prompt_tokens(seed, TIER_N))
     dt = time.perf_counter() - t0
     c.close()
     print(json.dumps({"store_s": dt, "stored_chunks": stored}), flush=True)

@@ -464,16 +464,29 @@ KV_API kv_status kv_tier_load(int fd, const kv_cache *cache, const int32_t *bloc
  *   kv_tier_store_prefix: reserve the prompt's whole chunks, store those not yet
  *     in the pool (runs of consecutive new chunks, one kv_store each; the
  *     partial last chunk is not kept), commit them after the stores completed,
- *     or abort them if a store failed.  *stored_chunks = chunks written.
+ *     or abort them all if a store failed.  With `state` (hybrid models, Sec.
+ *     2.2), page `state_page` of the replica's recurrent layers is the snapshot
+ *     at the boundary after the prompt's last whole chunk; it is stored into a
+ *     snapshot slot of the index unless that chunk already has one.
+ *     *stored_chunks = chunks written, *stored_state = 1 if a snapshot was
+ *     written (either may be NULL).
  *   kv_tier_load_prefix: the longest whole-chunk hit (Sec. 3.1-3.2: hits are
  *     whole chunks), pinned while it is loaded into the cache's first
- *     hit_tokens token slots.  *hit_tokens = hit chunks * C (0: nothing loaded).
- * block_table: HOST int32[ceil(n_tokens / BS)] for the whole prompt.  KV_EBUSY
- * if the index cannot free enough slots (nothing stored). */
-KV_API kv_status kv_tier_store_prefix(int fd, const kv_cache *cache, const int32_t *block_table, uint64_t salt,
+ *     hit_tokens token slots.  With `state` the hit follows aligned recovery
+ *     (Sec. 2.2): only a prefix whose boundary snapshot is present counts, and
+ *     that snapshot is loaded into page `state_page`.  *hit_tokens = hit chunks
+ *     * C (0: nothing loaded).
+ * block_table: HOST int32[ceil(n_tokens / BS)] for the whole prompt; state: as
+ * for kv_store_state (its buffers exported like the cache's), or NULL.  The
+ * tier's pool needs a state area of G*page_bytes slots for state requests, and
+ * its index as many snapshot slots at most.  KV_EBUSY if the index cannot free
+ * enough slots (then nothing was stored). */
+KV_API kv_status kv_tier_store_prefix(int fd, const kv_cache *cache, const int32_t *block_table,
+                                      const kv_state *state, int64_t state_page, uint64_t salt,
                                       const int32_t *tokens, int64_t n_tokens, int64_t *stored_chunks,
-                                      void *stream);
-KV_API kv_status kv_tier_load_prefix(int fd, const kv_cache *cache, const int32_t *block_table, uint64_t salt,
+                                      int32_t *stored_state, void *stream);
+KV_API kv_status kv_tier_load_prefix(int fd, const kv_cache *cache, const int32_t *block_table,
+                                     const kv_state *state, int64_t state_page, uint64_t salt,
                                      const int32_t *tokens, int64_t n_tokens, int64_t *hit_tokens, void *stream);
 
 /* Thread-local text of the last failure on this thread (HIP error name, message, call site). */

@@ -215,6 +215,7 @@ namespace kvx {
 
 int32_t index_chunk_tokens(const kv_index *index) { return index->C; }
 int64_t index_num_slots(const kv_index *index) { return index->num_slots; }
+int64_t index_num_state_slots(const kv_index *index) { return index->num_state_slots; }
 
 }  // namespace kvx
 

@@ -107,6 +107,7 @@ kv_status check_state_request(const kv_state *state, int64_t pool_state_slot_byt
 // Geometry of a pool index (for the tier's consistency check).
 int32_t index_chunk_tokens(const kv_index *index);
 int64_t index_num_slots(const kv_index *index);
+int64_t index_num_state_slots(const kv_index *index);
 
 }  // namespace kvx
 

@@ -50,6 +50,11 @@ struct RequestHeader {
     int64_t n_chunks;  // int64 chunk ids after the table (slot requests)
     int64_t n_ids;     // int32 token ids after the chunk ids (prefix requests)
     uint64_t salt;
+    // Recurrent-state pages (prefix requests of hybrid models): state_layers IPC buffers follow
+    // the cache's layers; the snapshot is page `page` of each.
+    int32_t state_layers;  // 0 = no state
+    int32_t pad2;
+    int64_t page_bytes, page_stride, num_pages, page;
 };
 
 struct ReplyHeader {
@@ -57,7 +62,8 @@ struct ReplyHeader {
     int32_t status;
     uint32_t msg_len;
     uint32_t pad;
-    int64_t value;  // chunks stored (store prefix) or tokens hit (load prefix)
+    int64_t value;   // chunks stored (store prefix) or tokens hit (load prefix)
+    int64_t value2;  // snapshots stored (store prefix)
 };
 
 // Whole-buffer socket I/O.  Returns false on EOF or error (errno kept); *eof set on a clean
@@ -132,38 +138,95 @@ class Connection {
                                  std::strerror(errno));
             }
             if (h.magic != kMagic || h.op < kOpStore || h.op > kOpLoadPrefix || h.num_layers < 1 ||
-                h.num_layers > kMaxLayers || h.n_table < 0 || h.n_chunks < 0 || h.n_ids < 0)
+                h.num_layers > kMaxLayers || h.n_table < 0 || h.n_chunks < 0 || h.n_ids < 0 ||
+                h.state_layers < 0 || h.state_layers > kMaxLayers)
                 return kvx::fail(KV_EINVAL, "tier: malformed request header");
-            const int64_t payload = static_cast<int64_t>(h.num_layers) * int64_t(sizeof(kv_ipc_buffer)) +
+            const int64_t payload = static_cast<int64_t>(h.num_layers + h.state_layers) * int64_t(sizeof(kv_ipc_buffer)) +
                                     h.n_table * int64_t(sizeof(int32_t)) + h.n_chunks * int64_t(sizeof(int64_t)) +
                                     h.n_ids * int64_t(sizeof(int32_t));
             if (payload > kMaxPayload)
                 return kvx::fail(KV_EINVAL, "tier: request payload of %lld bytes is too large",
                                  static_cast<long long>(payload));
             bufs_.resize(static_cast<size_t>(h.num_layers));
+            state_bufs_.resize(static_cast<size_t>(h.state_layers));
             table_host_.resize(static_cast<size_t>(h.n_table));
             ids_.resize(static_cast<size_t>(h.n_chunks));
             tokens_.resize(static_cast<size_t>(h.n_ids));
             if (!read_full(fd_, bufs_.data(), bufs_.size() * sizeof(kv_ipc_buffer)) ||
+                !read_full(fd_, state_bufs_.data(), state_bufs_.size() * sizeof(kv_ipc_buffer)) ||
                 !read_full(fd_, table_host_.data(), table_host_.size() * sizeof(int32_t)) ||
                 !read_full(fd_, ids_.data(), ids_.size() * sizeof(int64_t)) ||
                 !read_full(fd_, tokens_.data(), tokens_.size() * sizeof(int32_t)))
                 return kvx::fail(KV_EINVAL, "tier: connection failed while reading a request body");
 
             kv_status st;
-            int64_t value = 0;
+            int64_t value = 0, value2 = 0;
             {
                 std::lock_guard<std::mutex> lock(pool_->tier_mu);
-                st = execute(h, &value);
+                st = execute(h, &value, &value2);
             }
             const std::string msg = st == KV_OK ? std::string() : std::string(kv_last_error());
-            ReplyHeader r{kMagic, st, static_cast<uint32_t>(msg.size()), 0, value};
+            ReplyHeader r{kMagic, st, static_cast<uint32_t>(msg.size()), 0, value, value2};
             if (!write_full(fd_, &r, sizeof(r)) || !write_full(fd_, msg.data(), msg.size()))
                 return kvx::fail(KV_EINVAL, "tier: connection failed while replying (%s)", std::strerror(errno));
         }
     }
 
   private:
+    // Open (once per connection) the allocation behind an IPC buffer; *out = the buffer's address
+    // in this process if [offset, offset + need) lies inside the mapping opened here.
+    kv_status open_buffer(const kv_ipc_buffer &buf, int64_t need, const char *what, int32_t l, void **out) {
+        std::array<uint8_t, 64> key;
+        std::memcpy(key.data(), buf.handle, 64);
+        auto it = opened_.find(key);
+        if (it == opened_.end()) {
+            hipIpcMemHandle_t handle;
+            static_assert(sizeof(handle) == 64, "IPC handle size");
+            std::memcpy(&handle, buf.handle, 64);
+            void *base = nullptr;
+            KVX_HIP(hipIpcOpenMemHandle(&base, handle, hipIpcMemLazyEnablePeerAccess));
+            // The mapping's own size bounds every access (the peer's word is not trusted).
+            void *range_base = nullptr;
+            size_t size = 0;
+            const hipError_t e = hipMemGetAddressRange(&range_base, &size, base);
+            if (e != hipSuccess) {
+                (void)hipIpcCloseMemHandle(base);
+                return kvx::hip_fail(e, "hipMemGetAddressRange(opened IPC buffer)", __FILE__, __LINE__);
+            }
+            it = opened_.emplace(key, Mapping{base, static_cast<int64_t>(size)}).first;
+        }
+        if (buf.offset < 0 || need < 0 || buf.offset + need > it->second.bytes)
+            return kvx::fail(KV_EINVAL, "tier: %s %d (offset %lld, %lld bytes) exceeds its shared allocation of %lld "
+                                        "bytes",
+                             what, l, static_cast<long long>(buf.offset), static_cast<long long>(need),
+                             static_cast<long long>(it->second.bytes));
+        *out = static_cast<uint8_t *>(it->second.base) + buf.offset;
+        return KV_OK;
+    }
+
+    // The replica's recurrent-state pages as this process sees them.
+    kv_status map_state(const RequestHeader &h, kv_state *state) {
+        const int64_t stride = h.page_stride ? h.page_stride : h.page_bytes;
+        if (h.page_bytes < 1 || stride < h.page_bytes || h.num_pages < 1 || h.page < 0 || h.page >= h.num_pages ||
+            h.num_pages > INT64_MAX / stride)
+            return kvx::fail(KV_EINVAL, "tier: invalid recurrent-state pages");
+        state_layers_.resize(static_cast<size_t>(h.state_layers));
+        for (int32_t g = 0; g < h.state_layers; ++g) {
+            kv_status st = open_buffer(state_bufs_[g], (h.num_pages - 1) * stride + h.page_bytes, "state layer", g,
+                                       &state_layers_[static_cast<size_t>(g)]);
+            if (st != KV_OK)
+                return st;
+        }
+        std::memset(state, 0, sizeof(*state));
+        state->num_layers = h.state_layers;
+        state->device = pool_->device;
+        state->page_bytes = h.page_bytes;
+        state->page_stride = h.page_stride;
+        state->num_pages = h.num_pages;
+        state->layer_ptrs = state_layers_.data();
+        return KV_OK;
+    }
+
     // The replica's cache as this process sees it (layers mapped once per connection, each
     // bounded by the size of the mapping opened here), and its block table on the device.
     kv_status map_cache(const RequestHeader &h, kv_cache *cache) {
@@ -174,34 +237,14 @@ class Connection {
         if (h.block_stride_bytes < 0)
             return kvx::fail(KV_EINVAL, "tier: negative block stride");
         const kvx::Geometry g = kvx::geometry(lay, h.block_stride_bytes);
+        if (h.num_blocks < 1)
+            return kvx::fail(KV_EINVAL, "tier: num_blocks must be positive");
         layers_.resize(static_cast<size_t>(h.num_layers));
         for (int32_t l = 0; l < h.num_layers; ++l) {
-            std::array<uint8_t, 64> key;
-            std::memcpy(key.data(), bufs_[l].handle, 64);
-            auto it = opened_.find(key);
-            if (it == opened_.end()) {
-                hipIpcMemHandle_t handle;
-                static_assert(sizeof(handle) == 64, "IPC handle size");
-                std::memcpy(&handle, bufs_[l].handle, 64);
-                void *base = nullptr;
-                KVX_HIP(hipIpcOpenMemHandle(&base, handle, hipIpcMemLazyEnablePeerAccess));
-                // The mapping's own size bounds every access (the peer's word is not trusted).
-                void *range_base = nullptr;
-                size_t size = 0;
-                const hipError_t e = hipMemGetAddressRange(&range_base, &size, base);
-                if (e != hipSuccess) {
-                    (void)hipIpcCloseMemHandle(base);
-                    return kvx::hip_fail(e, "hipMemGetAddressRange(opened IPC buffer)", __FILE__, __LINE__);
-                }
-                it = opened_.emplace(key, Mapping{base, static_cast<int64_t>(size)}).first;
-            }
-            const int64_t need = bufs_[l].offset + static_cast<int64_t>(h.num_blocks) * g.block_stride;
-            if (bufs_[l].offset < 0 || h.num_blocks < 1 || need > it->second.bytes)
-                return kvx::fail(KV_EINVAL, "tier: layer %d (offset %lld, %d blocks of %lld bytes) exceeds its shared "
-                                            "allocation of %lld bytes",
-                                 l, static_cast<long long>(bufs_[l].offset), h.num_blocks,
-                                 static_cast<long long>(g.block_stride), static_cast<long long>(it->second.bytes));
-            layers_[static_cast<size_t>(l)] = static_cast<uint8_t *>(it->second.base) + bufs_[l].offset;
+            st = open_buffer(bufs_[l], static_cast<int64_t>(h.num_blocks) * g.block_stride, "layer", l,
+                             &layers_[static_cast<size_t>(l)]);
+            if (st != KV_OK)
+                return st;
         }
 
         // The block table into device memory on this connection's stream, from pinned host
@@ -252,7 +295,7 @@ class Connection {
         return KV_OK;
     }
 
-    kv_status execute(const RequestHeader &h, int64_t *value) {
+    kv_status execute(const RequestHeader &h, int64_t *value, int64_t *value2) {
         const kv_layout &lay = h.layout;
         if (lay.block_size < 1 || lay.chunk_tokens < 1 || h.n_tokens < 0 || lay.num_layers != h.num_layers)
             return kvx::fail(KV_EINVAL, "tier: request layout or length is invalid");
@@ -266,8 +309,11 @@ class Connection {
         if (prefix && !index_)
             return kvx::fail(KV_EINVAL, "tier: this tier serves no index, so it takes no prefix requests");
         if (prefix && (kvx::index_chunk_tokens(index_) != lay.chunk_tokens ||
-                       kvx::index_num_slots(index_) > pool_->num_slots))
-            return kvx::fail(KV_EINVAL, "tier: the index does not match the pool (chunk length or slot count)");
+                       kvx::index_num_slots(index_) > pool_->num_slots ||
+                       kvx::index_num_state_slots(index_) > pool_->num_state_slots))
+            return kvx::fail(KV_EINVAL, "tier: the index does not match the pool (chunk length or slot counts)");
+        if (h.state_layers && !prefix)
+            return kvx::fail(KV_EINVAL, "tier: recurrent state travels with prefix requests only");
         if (h.n_tokens == 0)
             return KV_OK;
 
@@ -275,6 +321,12 @@ class Connection {
         kv_status st = map_cache(h, &cache);
         if (st != KV_OK)
             return complete(st);
+        kv_state state;
+        if (h.state_layers) {
+            st = map_state(h, &state);
+            if (st != KV_OK)
+                return complete(st);
+        }
         (void)kv_pool_async_error(pool_, 1);
         switch (h.op) {
         case kOpStore:
@@ -282,13 +334,14 @@ class Connection {
         case kOpLoad:
             return complete(kv_load(&cache, table_, h.n_tokens, pool_, ids_.data(), stream_));
         case kOpStorePrefix:
-            return store_prefix(h, cache, value);
+            return store_prefix(h, cache, h.state_layers ? &state : nullptr, value, value2);
         default:
-            return load_prefix(h, cache, value);
+            return load_prefix(h, cache, h.state_layers ? &state : nullptr, value);
         }
     }
 
-    kv_status store_prefix(const RequestHeader &h, const kv_cache &cache, int64_t *stored) {
+    kv_status store_prefix(const RequestHeader &h, const kv_cache &cache, const kv_state *state, int64_t *stored,
+                           int64_t *stored_state) {
         const int64_t C = h.layout.chunk_tokens, bpc = C / h.layout.block_size;
         const int64_t nfull = h.n_tokens / C;
         slots_.resize(static_cast<size_t>(nfull));
@@ -313,25 +366,45 @@ class Connection {
                 count += b - a;
             a = b;
         }
+        // The snapshot at the boundary after the last whole chunk (Sec. 2.2), unless it has one.
+        int64_t state_slot = -1;
+        int32_t state_new = 0;
+        if (st == KV_OK && state && n_chunks > 0) {
+            st = kv_index_reserve_state(index_, slots_[n_chunks - 1], &state_slot, &state_new);
+            if (st == KV_OK && state_new)
+                st = kv_store_state(state, &h.page, 1, pool_, &state_slot, stream_);
+        }
         st = complete(st);
-        // Publish only chunks whose stores completed without fault (Sec. 3.2); else abort them all.
-        const kv_status commit = kv_index_commit(index_, slots_.data(), is_new_.data(), n_chunks, st == KV_OK);
+        // Publish only what completed without fault (Sec. 3.2); otherwise abort it all.
+        kv_status commit = KV_OK;
+        if (state_new)
+            commit = kv_index_commit_state(index_, slots_[n_chunks - 1], st == KV_OK);
+        const kv_status commit_chunks =
+            kv_index_commit(index_, slots_.data(), is_new_.data(), n_chunks, st == KV_OK);
         if (st != KV_OK)
             return st;
         if (commit != KV_OK)
             return commit;
+        if (commit_chunks != KV_OK)
+            return commit_chunks;
         *stored = count;
+        *stored_state = state_new;
         return KV_OK;
     }
 
-    kv_status load_prefix(const RequestHeader &h, const kv_cache &cache, int64_t *hit_tokens) {
+    kv_status load_prefix(const RequestHeader &h, const kv_cache &cache, const kv_state *state,
+                          int64_t *hit_tokens) {
         const int64_t nfull = h.n_tokens / h.layout.chunk_tokens;
         slots_.resize(static_cast<size_t>(nfull));
         kv_lookup hit;
-        kv_status st = kv_index_lookup(index_, h.salt, tokens_.data(), h.n_tokens, KV_LOOKUP_PIN, slots_.data(), &hit);
+        const uint32_t flags = KV_LOOKUP_PIN | (state ? KV_LOOKUP_REQUIRE_STATE : 0u);
+        kv_status st = kv_index_lookup(index_, h.salt, tokens_.data(), h.n_tokens, flags, slots_.data(), &hit);
         if (st != KV_OK)
             return complete(st);
         st = hit.hit_tokens ? kv_load(&cache, table_, hit.hit_tokens, pool_, slots_.data(), stream_) : KV_OK;
+        // Aligned recovery: the snapshot at the hit's boundary (the pinned last hit chunk keeps it).
+        if (st == KV_OK && state && hit.hit_chunks > 0)
+            st = kv_load_state(state, &h.page, 1, pool_, &hit.state_slot, stream_);
         st = complete(st);
         const kv_status unpin = kv_index_unpin(index_, slots_.data(), hit.hit_chunks);
         if (st != KV_OK)
@@ -354,18 +427,18 @@ class Connection {
         int64_t bytes;
     };
     std::map<std::array<uint8_t, 64>, Mapping> opened_;
-    std::vector<kv_ipc_buffer> bufs_;
+    std::vector<kv_ipc_buffer> bufs_, state_bufs_;
     std::vector<int32_t> table_host_;
     std::vector<int64_t> ids_;
     std::vector<int32_t> tokens_;
     std::vector<int64_t> slots_;
     std::vector<uint8_t> is_new_;
-    std::vector<void *> layers_;
+    std::vector<void *> layers_, state_layers_;
 };
 
 kv_status send_request(uint32_t op, int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
-                       const int64_t *chunk_ids, uint64_t salt, const int32_t *tokens, void *stream,
-                       int64_t *value) {
+                       const int64_t *chunk_ids, uint64_t salt, const int32_t *tokens, const kv_state *state,
+                       int64_t state_page, void *stream, int64_t *value, int64_t *value2) {
     if (!cache)
         return kvx::fail(KV_EINVAL, "cache must not be NULL");
     kv_status st = kvx::check_layout(cache->layout);
@@ -382,6 +455,10 @@ kv_status send_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
     const int32_t L = cache->layout.num_layers;
     if (L > kMaxLayers)
         return kvx::fail(KV_EUNSUPPORTED, "more than %d layers", kMaxLayers);
+    if (state && (state->num_layers < 1 || state->num_layers > kvx::kMaxStateLayers || !state->layer_ptrs ||
+                  state_page < 0 || state_page >= state->num_pages))
+        return kvx::fail(KV_EINVAL, "state needs 1..%d layers, layer pointers and a page in [0, num_pages)",
+                         kvx::kMaxStateLayers);
 
     // Host-side completion of everything enqueued before the call (Sec. 3.2).
     KVX_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
@@ -400,9 +477,18 @@ kv_status send_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
     h.n_chunks = prefix ? 0 : ceil_div(n_tokens, cache->layout.chunk_tokens);
     h.n_ids = prefix ? n_tokens : 0;
     h.salt = salt;
-    std::vector<kv_ipc_buffer> bufs(static_cast<size_t>(L));
-    for (int32_t l = 0; l < L; ++l) {
-        st = kv_ipc_export(cache->layer_ptrs[l], &bufs[static_cast<size_t>(l)]);
+    const int32_t G = state ? state->num_layers : 0;
+    if (state) {
+        h.state_layers = G;
+        h.page_bytes = state->page_bytes;
+        h.page_stride = state->page_stride;
+        h.num_pages = state->num_pages;
+        h.page = state_page;
+    }
+    std::vector<kv_ipc_buffer> bufs(static_cast<size_t>(L + G));
+    for (int32_t l = 0; l < L + G; ++l) {
+        const void *ptr = l < L ? cache->layer_ptrs[l] : state->layer_ptrs[l - L];
+        st = kv_ipc_export(ptr, &bufs[static_cast<size_t>(l)]);
         if (st != KV_OK)
             return st;
     }
@@ -423,6 +509,8 @@ kv_status send_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
     }
     if (value)
         *value = r.value;
+    if (value2)
+        *value2 = r.value2;
     return KV_OK;
 }
 
@@ -522,29 +610,35 @@ kv_status kv_tier_run(kv_pool *pool, kv_index *index, int listen_fd, int32_t con
 
 kv_status kv_tier_store(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                         const int64_t *chunk_ids, void *stream) {
-    return send_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, stream, nullptr);
+    return send_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream, nullptr,
+                        nullptr);
 }
 
 kv_status kv_tier_load(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                        const int64_t *chunk_ids, void *stream) {
-    return send_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, stream, nullptr);
+    return send_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream, nullptr,
+                        nullptr);
 }
 
-kv_status kv_tier_store_prefix(int fd, const kv_cache *cache, const int32_t *block_table, uint64_t salt,
-                               const int32_t *tokens, int64_t n_tokens, int64_t *stored_chunks, void *stream) {
-    int64_t v = 0;
-    const kv_status st =
-        send_request(kOpStorePrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, stream, &v);
+kv_status kv_tier_store_prefix(int fd, const kv_cache *cache, const int32_t *block_table, const kv_state *state,
+                               int64_t state_page, uint64_t salt, const int32_t *tokens, int64_t n_tokens,
+                               int64_t *stored_chunks, int32_t *stored_state, void *stream) {
+    int64_t v = 0, v2 = 0;
+    const kv_status st = send_request(kOpStorePrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, state,
+                                      state_page, stream, &v, &v2);
     if (stored_chunks)
         *stored_chunks = st == KV_OK ? v : 0;
+    if (stored_state)
+        *stored_state = st == KV_OK ? static_cast<int32_t>(v2) : 0;
     return st;
 }
 
-kv_status kv_tier_load_prefix(int fd, const kv_cache *cache, const int32_t *block_table, uint64_t salt,
-                              const int32_t *tokens, int64_t n_tokens, int64_t *hit_tokens, void *stream) {
+kv_status kv_tier_load_prefix(int fd, const kv_cache *cache, const int32_t *block_table, const kv_state *state,
+                              int64_t state_page, uint64_t salt, const int32_t *tokens, int64_t n_tokens,
+                              int64_t *hit_tokens, void *stream) {
     int64_t v = 0;
-    const kv_status st =
-        send_request(kOpLoadPrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, stream, &v);
+    const kv_status st = send_request(kOpLoadPrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, state,
+                                      state_page, stream, &v, nullptr);
     if (hit_tokens)
         *hit_tokens = st == KV_OK ? v : 0;
     return st;

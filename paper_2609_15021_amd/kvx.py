@@ -134,10 +134,10 @@ def _open():
         "kv_tier_serve": ([P, P, ctypes.c_int], i32),
         "kv_tier_listen": ([ctypes.c_char_p, ctypes.POINTER(ctypes.c_int)], i32),
         "kv_tier_run": ([P, P, ctypes.c_int, i32], i32),
-        "kv_tier_store_prefix": ([ctypes.c_int, ctypes.POINTER(KvCache), P, ctypes.c_uint64, P, i64,
-                                  ctypes.POINTER(i64), P], i32),
-        "kv_tier_load_prefix": ([ctypes.c_int, ctypes.POINTER(KvCache), P, ctypes.c_uint64, P, i64,
-                                 ctypes.POINTER(i64), P], i32),
+        "kv_tier_store_prefix": ([ctypes.c_int, ctypes.POINTER(KvCache), P, ctypes.POINTER(KvState), i64,
+                                  ctypes.c_uint64, P, i64, ctypes.POINTER(i64), ctypes.POINTER(i32), P], i32),
+        "kv_tier_load_prefix": ([ctypes.c_int, ctypes.POINTER(KvCache), P, ctypes.POINTER(KvState), i64,
+                                 ctypes.c_uint64, P, i64, ctypes.POINTER(i64), P], i32),
         "kv_tier_store": ([ctypes.c_int, ctypes.POINTER(KvCache), P, i64, P, P], i32),
         "kv_tier_load": ([ctypes.c_int, ctypes.POINTER(KvCache), P, i64, P, P], i32),
         "kv_last_error": ([], ctypes.c_char_p),
@@ -562,21 +562,31 @@ def kv_tier_load(fd: int, cache: Cache, block_table, n_tokens: int, chunk_ids, s
     _raise(_lib.kv_tier_load(int(fd), ctypes.byref(cache.struct), tp, int(n_tokens), ip, _stream_handle(stream)))
 
 
-def kv_tier_store_prefix(fd: int, cache: Cache, block_table, salt: int, tokens, stream=None) -> int:
-    """Store the prompt's whole chunks that the tier does not hold yet; returns the chunks stored."""
+def kv_tier_store_prefix(fd: int, cache: Cache, block_table, salt: int, tokens, stream=None, state: State = None,
+                         state_page: int = 0):
+    """Store the prompt's whole chunks that the tier does not hold yet (and, with ``state``, the
+    snapshot in page ``state_page`` at the prompt's last whole-chunk boundary); returns
+    (chunks stored, snapshots stored)."""
+    t, tp = _host_table(block_table)
+    tok, kp = _tokens(tokens)
+    out, out_state = ctypes.c_int64(), ctypes.c_int32()
+    _raise(_lib.kv_tier_store_prefix(int(fd), ctypes.byref(cache.struct), tp,
+                                     ctypes.byref(state.struct) if state is not None else None, int(state_page),
+                                     int(salt) & 0xFFFFFFFFFFFFFFFF, kp, int(tok.size), ctypes.byref(out),
+                                     ctypes.byref(out_state), _stream_handle(stream)))
+    return int(out.value), int(out_state.value)
+
+
+def kv_tier_load_prefix(fd: int, cache: Cache, block_table, salt: int, tokens, stream=None, state: State = None,
+                        state_page: int = 0) -> int:
+    """Load the prompt's longest whole-chunk hit into the cache (with ``state``: the longest hit
+    under aligned recovery, and its boundary snapshot into page ``state_page``); returns the hit
+    tokens."""
     t, tp = _host_table(block_table)
     tok, kp = _tokens(tokens)
     out = ctypes.c_int64()
-    _raise(_lib.kv_tier_store_prefix(int(fd), ctypes.byref(cache.struct), tp, int(salt) & 0xFFFFFFFFFFFFFFFF, kp,
-                                     int(tok.size), ctypes.byref(out), _stream_handle(stream)))
-    return int(out.value)
-
-
-def kv_tier_load_prefix(fd: int, cache: Cache, block_table, salt: int, tokens, stream=None) -> int:
-    """Load the prompt's longest whole-chunk hit into the cache; returns the hit tokens."""
-    t, tp = _host_table(block_table)
-    tok, kp = _tokens(tokens)
-    out = ctypes.c_int64()
-    _raise(_lib.kv_tier_load_prefix(int(fd), ctypes.byref(cache.struct), tp, int(salt) & 0xFFFFFFFFFFFFFFFF, kp,
-                                    int(tok.size), ctypes.byref(out), _stream_handle(stream)))
+    _raise(_lib.kv_tier_load_prefix(int(fd), ctypes.byref(cache.struct), tp,
+                                    ctypes.byref(state.struct) if state is not None else None, int(state_page),
+                                    int(salt) & 0xFFFFFFFFFFFFFFFF, kp, int(tok.size), ctypes.byref(out),
+                                    _stream_handle(stream)))
     return int(out.value)

@@ -216,7 +216,7 @@ def test_prefix_store_and_external_hit(mode, tmp_path):
         c2 = _connect(sock)                  # a third replica re-stores the same prompt: nothing new
         dC = torch.zeros_like(dB)
         torch.cuda.synchronize()
-        assert kvx.kv_tier_store_prefix(c2.fileno(), kvx.Cache(dC, lay.kv, NB), btB, salt, tokens) == 0
+        assert kvx.kv_tier_store_prefix(c2.fileno(), kvx.Cache(dC, lay.kv, NB), btB, salt, tokens) == (0, 0)
         c2.close()
     finally:
         out = _finish_native(tier)
@@ -257,3 +257,52 @@ def test_prefix_eviction_under_a_small_pool(tmp_path):
     finally:
         out = _finish_native(tier)
     assert "'evictions': 2" in out
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_hybrid_prefix_aligned_recovery_across_processes(mode, tmp_path):
+    """The paper's hybrid case through the tier (Sec. 2.2): replica A stores a prompt's whole
+    chunks plus the recurrent snapshot at its last whole-chunk boundary.  Replica B restores the
+    prompt with aligned recovery: chunks and snapshot, bit-exact.  A prompt that diverges inside
+    chunk 3 still shares 3 chunks of K/V pages but no snapshot at their boundary, so under aligned
+    recovery it is no hit at all (attention pages alone do not recover the hybrid state), while an
+    attention-only request hits the 3 chunks."""
+    from tests.tier_roles import state_pages
+    lay = TINY
+    n = 5 * lay.C + 100
+    NB = lay.nblk(n) + 9
+    G, pb, npages, page_a, page_b = 3, 8192, 4, 2, 1
+    seed, salt = harness.sub_seed("hybrid-tier", mode), 21
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    tier = _start_tier(sock, lay, 8, mode, 2, dump, role="tier-native", extra=("8", "2", str(G * pb)))
+    try:
+        r = subprocess.run([sys.executable, "-u", ROLES, "store-hybrid", sock, *_dims(lay), str(NB), str(n), str(seed),
+                            str(salt), str(G), str(pb), str(npages), str(page_a)],
+                           capture_output=True, text=True, timeout=120)
+        assert r.returncode == 0 and "STORED 5 1" in r.stdout, (r.stdout + r.stderr)[-3000:]
+        tokens = harness.prompt_tokens(seed, n)
+        btB = harness.block_table(seed + 2, NB, lay.nblk(n))
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
+        dS = torch.zeros((G, npages, pb), dtype=torch.uint8, device=DEV)
+        cB, sB = kvx.Cache(dB, lay.kv, NB), kvx.State(dS, pb, npages)
+        torch.cuda.synchronize()
+        c = _connect(sock)
+        hit = kvx.kv_tier_load_prefix(c.fileno(), cB, btB, salt, tokens, state=sB, state_page=page_b)
+        got_B, got_S = dB.cpu(), dS.cpu().numpy()
+        other = tokens.copy()
+        other[3 * lay.C + 7] ^= 1
+        assert kvx.kv_tier_load_prefix(c.fileno(), cB, btB, salt, other, state=sB, state_page=page_b) == 0
+        assert kvx.kv_tier_load_prefix(c.fileno(), cB, btB, salt, other) == 3 * lay.C
+        c.close()
+    finally:
+        _finish_native(tier)
+    assert hit == 5 * lay.C
+    A = host_cache(lay, NB, seed, "raw")
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+    want_pool = oracle_pool(lay, A, btA, hit, np.arange(5), 8, POOL_SENT)
+    want_B = oracle_unpack_into(lay, np.zeros_like(A), btB, hit, want_pool, np.arange(5))
+    got = got_B.numpy().view(A.dtype).reshape(A.shape)
+    assert np.array_equal(got, want_B), first_mismatch(got, want_B)
+    pages_A = state_pages(seed, G, npages, pb)
+    assert np.array_equal(got_S[:, page_b], pages_A[:, page_a])
+    assert not got_S[:, [p for p in range(npages) if p != page_b]].any()

@@ -10,6 +10,9 @@
                                                   writes byte 37 on its stream), stored through the tier
   store-prefix SOCK L H D E BS C NB N SEED SALT    replica A stores the prompt harness.prompt_tokens(SEED, N)
                                                   by prefix; prints the chunks it stored
+  store-hybrid (store-prefix arguments) G PB NPAGES PAGE
+                                                  the same plus recurrent-state pages (state_pages(SEED, ...))
+                                                  whose page PAGE is the snapshot after the last whole chunk
 """
 import os
 import socket
@@ -63,12 +66,18 @@ def tier(sock, L, H, D, E, BS, C, slots, mode, nconn, dump):
     kvx.kv_pool_destroy(pool)
 
 
-def tier_native(sock, L, H, D, E, BS, C, slots, mode, nconn, dump, index_slots):
+def state_pages(seed, G, npages, pb):
+    """Seeded recurrent-state pages [G][npages][pb] (uint8)."""
+    return np.random.default_rng(seed + 77).integers(0, 256, size=(G, npages, pb), dtype=np.uint8)
+
+
+def tier_native(sock, L, H, D, E, BS, C, slots, mode, nconn, dump, index_slots, state_slots=0, state_bytes=0):
     lay = kvx.make_layout(L, H, D, E, BS, C)
-    pool = kvx.kv_pool_create(lay, slots, mode, staging_slots=2, chunks_per_batch=2)
+    pool = kvx.kv_pool_create(lay, slots, mode, staging_slots=2, chunks_per_batch=2, num_state_slots=state_slots,
+                              state_slot_bytes=state_bytes)
     view = kvx.pool_view(pool)
     view[:] = POOL_SENT
-    index = kvx.kv_index_create(C, index_slots) if index_slots else None
+    index = kvx.kv_index_create(C, index_slots, state_slots) if index_slots else None
     fd = kvx.kv_tier_listen(sock)
     print("READY", flush=True)
     try:
@@ -97,9 +106,22 @@ def store_prefix(sock, L, H, D, E, BS, C, NB, n, seed, salt):
     bt = harness.block_table(seed + 1, NB, -(-n // BS))
     c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
     c.connect(sock)
-    stored = kvx.kv_tier_store_prefix(c.fileno(), cache, bt, salt, harness.prompt_tokens(seed, n))
+    stored, _ = kvx.kv_tier_store_prefix(c.fileno(), cache, bt, salt, harness.prompt_tokens(seed, n))
     c.close()
     print("STORED", stored, flush=True)
+
+
+def store_hybrid(sock, L, H, D, E, BS, C, NB, n, seed, salt, G, pb, npages, page):
+    dA, cache = replica_cache(L, H, D, E, BS, C, NB, seed)
+    dS = torch.from_numpy(state_pages(seed, G, npages, pb)).to("cuda:0")
+    torch.cuda.synchronize()
+    bt = harness.block_table(seed + 1, NB, -(-n // BS))
+    c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    c.connect(sock)
+    stored, stored_state = kvx.kv_tier_store_prefix(c.fileno(), cache, bt, salt, harness.prompt_tokens(seed, n),
+                                                    state=kvx.State(dS, pb, npages), state_page=page)
+    c.close()
+    print("STORED", stored, stored_state, flush=True)
 
 
 def store(sock, L, H, D, E, BS, C, NB, n, seed, delay_ms):
@@ -127,10 +149,12 @@ if __name__ == "__main__":
     if role == "tier":
         tier(args[0], *map(int, args[1:8]), args[8], int(args[9]), args[10])
     elif role == "tier-native":
-        tier_native(args[0], *map(int, args[1:8]), args[8], int(args[9]), args[10], int(args[11]))
+        tier_native(args[0], *map(int, args[1:8]), args[8], int(args[9]), args[10], *map(int, args[11:]))
     elif role == "store":
         store(args[0], *map(int, args[1:12]))
     elif role == "store-prefix":
         store_prefix(args[0], *map(int, args[1:12]))
+    elif role == "store-hybrid":
+        store_hybrid(args[0], *map(int, args[1:16]))
     else:
         raise SystemExit(f"unknown role {role}")

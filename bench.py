@@ -65,6 +65,11 @@ def parse():
     ap.add_argument("--no-tier", action="store_true", help="skip the cross-process (tier) measurement")
     ap.add_argument("--tier-only", action="store_true",
                     help="only measure store/restore between processes through a tier (run by the main bench)")
+    ap.add_argument("--no-paper-hybrid", action="store_true", help="skip the paper's hybrid prompt through the tier")
+    ap.add_argument("--paper-hybrid-only", action="store_true",
+                    help="only measure the paper's hybrid 128k prompt through the tier (run by the main bench)")
+    ap.add_argument("--paper-hybrid-server", metavar="SOCKET", help=argparse.SUPPRESS)
+    ap.add_argument("--paper-hybrid-store", metavar="SOCKET", help=argparse.SUPPRESS)
     ap.add_argument("--tier-server", metavar="SOCKET", help=argparse.SUPPRESS)
     ap.add_argument("--tier-store", metavar="SOCKET", help=argparse.SUPPRESS)
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -478,6 +483,135 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
             "round_trip": msg if ok else f"FAILED: {msg}"}, ok
 
 
+# The paper's hybrid deployment (Table 1, Sec. 2.2, Sec. 3.1-3.2): 16 full-attention layers of
+# FP8-sized K/V (4 KV heads, head_dim 256, 32-token HND pages), 1,568-token chunks, 48 recurrent
+# layers with one boundary snapshot page each (the page size is an assumption), and a 128,000-token
+# prompt, whose whole chunks are the 127,008 tokens the paper's replica B hit externally.
+PH = dict(L=16, H=4, D=256, E=1, BS=32, C=1568, N=128000, NB=4096)
+
+
+def paper_hybrid_cache(torch, hg, kvx, dev, seed=None, state_seed=None):
+    L_, H_, D_, BS_ = PH["L"], PH["H"], PH["D"], PH["BS"]
+    lay = kvx.make_layout(L_, H_, D_, PH["E"], BS_, PH["C"])
+    block_elems = 2 * H_ * BS_ * D_
+    layers = [torch.empty((PH["NB"], 2, H_, BS_, D_), dtype=torch.uint8, device=dev) for _ in range(L_)]
+    pages = [torch.empty((2, GDN_PAGE), dtype=torch.uint8, device=dev) for _ in range(GDN_LAYERS)]
+    for l, t in enumerate(layers):
+        if seed is None:
+            t.zero_()
+        else:
+            hg.fill_values(t, l * PH["NB"] * block_elems, seed, "raw", 1)
+    for g, t in enumerate(pages):
+        if state_seed is None:
+            t.zero_()
+        else:
+            hg.fill_values(t, g * 2 * GDN_PAGE, state_seed, "raw", 1)
+    torch.cuda.synchronize()
+    return layers, pages, kvx.Cache(layers, lay, PH["NB"]), kvx.State(pages, GDN_PAGE, 2)
+
+
+def paper_hybrid_server(kvx, sock, mode):
+    lay = kvx.make_layout(PH["L"], PH["H"], PH["D"], PH["E"], PH["BS"], PH["C"])
+    slots = -(-PH["N"] // PH["C"])
+    pool = kvx.kv_pool_create(lay, slots, mode, num_state_slots=2, state_slot_bytes=GDN_LAYERS * GDN_PAGE)
+    index = kvx.kv_index_create(PH["C"], slots, 2)
+    fd = kvx.kv_tier_listen(sock)
+    print("READY", flush=True)
+    errors = []
+    try:
+        kvx.kv_tier_run(pool, fd, 2, index)
+    except kvx.KvError as e:
+        errors.append(repr(e))
+    os.close(fd)
+    stats = kvx.kv_index_get_stats(index)
+    kvx.kv_pool_destroy(pool)
+    print(json.dumps({"errors": errors, "index": stats}), flush=True)
+    sys.exit(1 if errors else 0)
+
+
+def paper_hybrid_store(torch, harness, hg, kvx, sock, dev):
+    import socket
+    seed = harness.sub_seed("bench-paper-hybrid")
+    _, _, cache, state = paper_hybrid_cache(torch, hg, kvx, dev, seed, seed + 7)
+    bt = harness.block_table(seed + 1, PH["NB"], -(-PH["N"] // PH["BS"]))
+    c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+    c.connect(sock)
+    t0 = time.perf_counter()
+    stored, stored_state = kvx.kv_tier_store_prefix(c.fileno(), cache, bt, 3, harness.prompt_tokens(seed, PH["N"]),
+                                                    state=state, state_page=1)
+    dt = time.perf_counter() - t0
+    c.close()
+    print(json.dumps({"store_s": dt, "stored_chunks": stored, "stored_state": stored_state}), flush=True)
+
+
+def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
+    """Replica A stores the paper's 128,000-token hybrid prompt through the tier (chunks and the
+    boundary snapshot); replica B asks for the same prompt under aligned recovery."""
+    import socket
+    import subprocess
+    import tempfile
+    sock = os.path.join(tempfile.mkdtemp(prefix="kvx_ph_"), "tier.sock")
+    me = os.path.abspath(__file__)
+    tier = subprocess.Popen([sys.executable, "-u", me, "--paper-hybrid-server", sock, "--mode", mode],
+                            stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+    try:
+        if not tier.stdout.readline().startswith("READY"):
+            raise RuntimeError("tier did not start: " + tier.stderr.read()[-2000:])
+        r = subprocess.run([sys.executable, "-u", me, "--paper-hybrid-store", sock], capture_output=True, text=True,
+                           timeout=300)
+        if r.returncode != 0:
+            raise RuntimeError("replica A failed: " + r.stderr[-2000:])
+        a_out = json.loads(r.stdout.strip().splitlines()[-1])
+        seed = harness.sub_seed("bench-paper-hybrid")
+        layers_b, pages_b, cache_b, state_b = paper_hybrid_cache(torch, hg, kvx, dev)
+        nblk = -(-PH["N"] // PH["BS"])
+        bt_a = harness.block_table(seed + 1, PH["NB"], nblk)
+        bt_b = harness.block_table(seed + 2, PH["NB"], nblk)
+        prompt = harness.prompt_tokens(seed, PH["N"])
+        c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
+        c.connect(sock)
+        restore, hits = [], []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            hits.append(kvx.kv_tier_load_prefix(c.fileno(), cache_b, bt_b, 3, prompt, state=state_b, state_page=0))
+            restore.append(time.perf_counter() - t0)
+        c.close()
+        out, err = tier.communicate(timeout=120)
+        if tier.returncode != 0:
+            raise RuntimeError("tier failed: " + (out + err)[-2000:])
+        tier_out = json.loads(out.strip().splitlines()[-1])
+    finally:
+        if tier.poll() is None:
+            tier.kill()
+    # Checks: the snapshot pages equal A's page 1 (regenerated), and sampled hit chunks equal A's
+    # source blocks (regenerated from the seeded generator).
+    ok = all(h == 127008 for h in hits) and a_out["stored_chunks"] == 81 and a_out["stored_state"] == 1
+    ref = torch.empty((2, GDN_PAGE), dtype=torch.uint8, device=dev)
+    for g, t in enumerate(pages_b):
+        hg.fill_values(ref, g * 2 * GDN_PAGE, seed + 7, "raw", 1)
+        torch.cuda.synchronize()
+        ok = ok and bool(torch.equal(t[0], ref[1])) and not bool(t[1].any())
+    bpc = PH["C"] // PH["BS"]
+    for i in (0, 40, 80):
+        blocks_a = bt_a[i * bpc:(i + 1) * bpc]
+        src = harness.gen_blocks(seed, "raw", PH["L"], PH["NB"], PH["H"], PH["BS"], PH["D"], PH["E"], blocks=blocks_a)
+        idx = torch.from_numpy(bt_b[i * bpc:(i + 1) * bpc].astype(np.int64)).to(dev)
+        got = torch.stack([t[idx] for t in layers_b]).cpu().numpy()
+        ok = ok and np.array_equal(got, src.reshape(got.shape))
+    attn = 127008 * 2 * PH["L"] * PH["H"] * PH["D"] * PH["E"]
+    snap = GDN_LAYERS * GDN_PAGE
+    med = statistics.median(restore[1:] or restore)
+    return {"workload": "the paper's hybrid deployment through the tier, 3 processes: 16 FP8-sized attention layers "
+                        "(4 KV heads, head_dim 256, 32-token HND pages), 1,568-token chunks, 48 recurrent layers with "
+                        "3 MiB + 60 KiB snapshot pages; a 128,000-token prompt stored by replica A with its boundary "
+                        "snapshot and restored by replica B under aligned recovery",
+            "mode": mode, "external_hit_tokens": hits[0], "stored_chunks": a_out["stored_chunks"],
+            "bytes_restored": attn + snap, "store_s": round(a_out["store_s"], 4),
+            "restore_s_first": round(restore[0], 4), "restore_s": round(med, 4),
+            "restore_GBps": round((attn + snap) / med / 1e9, 3), "tier_index": tier_out["index"],
+            "round_trip": "bit-exact (sampled chunks 0, 40, 80 and all snapshot pages)" if ok else "FAILED"}, ok
+
+
 def cpu_baseline(np, oracle, n_chunks=64):
     """The oracle timed on host cores: store + load of a bounded sample of the workload."""
     rng = np.random.default_rng(2609)
@@ -536,6 +670,16 @@ def main():
         res, res_ok = state_snapshots(np, torch, hg, kvx, args.mode, dev)
         print(json.dumps(res), flush=True)
         sys.exit(0 if res_ok else 1)
+    if args.paper_hybrid_server:
+        paper_hybrid_server(kvx, args.paper_hybrid_server, args.mode)
+        return
+    if args.paper_hybrid_store:
+        paper_hybrid_store(torch, harness, hg, kvx, args.paper_hybrid_store, dev)
+        return
+    if args.paper_hybrid_only:
+        res, res_ok = paper_hybrid_leg(np, torch, harness, hg, kvx, "zero_copy", dev)
+        print(json.dumps(res), flush=True)
+        sys.exit(0 if res_ok else 1)
     if args.tier_server:
         tier_server(torch, kvx, args.tier_server, args.mode)
         return
@@ -584,7 +728,14 @@ def main():
                 log(f"[bench] tier ({m}, 3 processes): {t['external_hit_tokens']} tokens hit; store {t['store_s']} s ({t['store_GBps']} GB/s), restore "
                     f"{t['restore_s']} s ({t['restore_GBps']} GB/s, first {t['restore_s_first']} s); "
                     f"{t['round_trip']}")
-    paper_ok = paper_ok and state_ok and tier_ok
+    hybrid, hybrid_ok = None, True
+    if not args.no_paper_hybrid:
+        hybrid, hybrid_ok = child_leg("--paper-hybrid-only")
+        if "error" not in hybrid:
+            log(f"[bench] paper hybrid prompt through the tier: {hybrid['external_hit_tokens']} tokens hit + snapshot, "
+                f"restore {hybrid['restore_s']} s ({hybrid['restore_GBps']} GB/s), store {hybrid['store_s']} s; "
+                f"{hybrid['round_trip']}")
+    paper_ok = paper_ok and state_ok and tier_ok and hybrid_ok
 
     layout = kvx.make_layout(L, H, D, E, BS, C)
     n = args.tokens
@@ -780,6 +931,7 @@ def main():
         "paper_layout": paper,
         "state_snapshots": state,
         "tier": tier,
+        "paper_hybrid_tier": hybrid,
         "pool_index": index,
         "cpu_baseline": cpu,
     }

@@ -5,6 +5,7 @@ Three processes on the GPU: the tier owns the pinned pool; replica A (a child pr
 its prefix through the tier; replica B (this test) loads it into a fresh fragmented block set.
 The pool bytes (dumped by the tier) and B's cache are compared with the oracle.
 """
+import contextlib
 import os
 import socket
 import subprocess
@@ -20,6 +21,16 @@ from paper_2609_15021_amd import kvx
 from tests.gpu_support import DEV, TINY, first_mismatch, host_cache, oracle_pool, oracle_unpack_into, to_host
 
 pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _fresh_segments():
+    """Buffers shared with the tier must be their own allocations under 2 GiB: release the caching
+    allocator's free segments first (earlier tests leave huge ones that small tensors would be
+    carved from, and kv_ipc_export rightly refuses to share those)."""
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    yield
 
 ROLES = os.path.join(os.path.dirname(os.path.abspath(__file__)), "tier_roles.py")
 POOL_SENT = 0xA5
@@ -59,7 +70,27 @@ def _store_process(sock, lay, NB, n, seed, delay_ms):
 def _connect(sock):
     c = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
     c.connect(sock)
+    _OPEN.append(c)
     return c
+
+
+_OPEN = []  # sockets of the running test, closed if it fails
+
+
+@contextlib.contextmanager
+def _serving(tier):
+    """Run a test body against a started tier: on any failure close the test's sockets and kill
+    the tier, so the original error surfaces instead of a wait for connections that never come."""
+    _OPEN.clear()
+    try:
+        yield tier
+    except BaseException:
+        for c in _OPEN:
+            c.close()
+        tier.kill()
+        out, _ = tier.communicate(timeout=30)
+        print("tier output:", (out or "")[-3000:])  # shown by pytest with the failure
+        raise
 
 
 @pytest.mark.parametrize("mode", ["zero_copy", "staged"])
@@ -70,7 +101,7 @@ def test_two_replica_processes_share_one_pool(mode, tmp_path):
     seed = harness.sub_seed("tier", mode)
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
     tier = _start_tier(sock, lay, nc + 2, mode, 2, dump)
-    try:
+    with _serving(tier):
         _store_process(sock, lay, NB, n, seed, 0)
         btB = harness.block_table(seed + 2, NB, lay.nblk(n))
         dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
@@ -80,8 +111,7 @@ def test_two_replica_processes_share_one_pool(mode, tmp_path):
         kvx.kv_tier_load(c.fileno(), kvx.Cache(dB, lay.kv, NB), btB, n, np.arange(nc), s)
         got_B = dB.cpu()  # the load completed before kv_tier_load returned
         c.close()
-    finally:
-        _finish_tier(tier)
+    _finish_tier(tier)
     A = host_cache(lay, NB, seed, "raw")
     btA = harness.block_table(seed + 1, NB, lay.nblk(n))
     want_pool = oracle_pool(lay, A, btA, n, np.arange(nc), nc + 2, POOL_SENT)
@@ -101,10 +131,9 @@ def test_delayed_producer_across_processes(mode, tmp_path):
     nc, NB = lay.nc(n), lay.nblk(n) + 4
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
     tier = _start_tier(sock, lay, nc, mode, 1, dump)
-    try:
+    with _serving(tier):
         _store_process(sock, lay, NB, n, harness.sub_seed("tier-37", mode), 60)
-    finally:
-        _finish_tier(tier)
+    _finish_tier(tier)
     pool = np.load(dump)
     assert pool.size == nc * lay.slot_bytes and (pool == 37).all()
 
@@ -115,7 +144,7 @@ def test_tier_rejects_a_bad_request_and_keeps_serving(tmp_path):
     nc, NB = lay.nc(n), 64
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
     tier = _start_tier(sock, lay, nc, "staged", 1, dump)
-    try:
+    with _serving(tier):
         dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
         cache = kvx.Cache(dB, lay.kv, NB)
         bt = np.arange(lay.nblk(n), dtype=np.int32)
@@ -130,8 +159,7 @@ def test_tier_rejects_a_bad_request_and_keeps_serving(tmp_path):
         assert e.value.status == kvx.KV_EINVAL and "exceeds its shared allocation" in str(e.value)
         kvx.kv_tier_load(c.fileno(), cache, bt, n, np.arange(nc), None)  # still served
         c.close()
-    finally:
-        _finish_tier(tier)
+    _finish_tier(tier)
 
 
 def test_ipc_export_refuses_allocations_of_2_gib():
@@ -154,7 +182,7 @@ def test_tier_survives_a_malformed_connection(tmp_path):
     nc, NB = lay.nc(n), 64
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
     p = _start_tier(sock, lay, nc, "staged", 2, dump)
-    try:
+    with _serving(p):
         bad = _connect(sock)
         bad.sendall(b"\x00" * 160)  # a full header's worth of bytes with the wrong magic
         bad.close()
@@ -164,9 +192,6 @@ def test_tier_survives_a_malformed_connection(tmp_path):
                          np.arange(nc), None)
         c.close()
         out, _ = p.communicate(timeout=90)
-    finally:
-        if p.poll() is None:
-            p.kill()
     assert p.returncode == 0, out[-2000:]
     results = [ln for ln in out.splitlines() if ln.startswith("TIER")][-1].split(" ", 1)[1].split(";")
     assert sorted(r == "ok" for r in results) == [False, True], results
@@ -196,7 +221,7 @@ def test_prefix_store_and_external_hit(mode, tmp_path):
     seed, salt = harness.sub_seed("prefix", mode), 11
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
     tier = _start_native_tier(sock, lay, 8, mode, 3, dump, 8)
-    try:
+    with _serving(tier):
         r = subprocess.run([sys.executable, "-u", ROLES, "store-prefix", sock, *_dims(lay), str(NB), str(n), str(seed),
                             str(salt)], capture_output=True, text=True, timeout=120)
         assert r.returncode == 0 and "STORED 5" in r.stdout, (r.stdout + r.stderr)[-3000:]
@@ -218,8 +243,7 @@ def test_prefix_store_and_external_hit(mode, tmp_path):
         torch.cuda.synchronize()
         assert kvx.kv_tier_store_prefix(c2.fileno(), kvx.Cache(dC, lay.kv, NB), btB, salt, tokens) == (0, 0)
         c2.close()
-    finally:
-        out = _finish_native(tier)
+    out = _finish_native(tier)
     assert hit == 5 * lay.C
     A = host_cache(lay, NB, seed, "raw")
     btA = harness.block_table(seed + 1, NB, lay.nblk(n))
@@ -241,7 +265,7 @@ def test_prefix_eviction_under_a_small_pool(tmp_path):
     NB = lay.nblk(n) + 4
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
     tier = _start_native_tier(sock, lay, 4, "staged", 3, dump, 4)
-    try:
+    with _serving(tier):
         for seed in (101, 202):
             r = subprocess.run([sys.executable, "-u", ROLES, "store-prefix", sock, *_dims(lay), str(NB), str(n),
                                 str(seed), "5"], capture_output=True, text=True, timeout=120)
@@ -254,8 +278,7 @@ def test_prefix_eviction_under_a_small_pool(tmp_path):
         assert kvx.kv_tier_load_prefix(c.fileno(), cB, bt, 5, harness.prompt_tokens(101, n)) == 1 * lay.C
         assert kvx.kv_tier_load_prefix(c.fileno(), cB, bt, 5, harness.prompt_tokens(202, n)) == 3 * lay.C
         c.close()
-    finally:
-        out = _finish_native(tier)
+    out = _finish_native(tier)
     assert "'evictions': 2" in out
 
 
@@ -275,7 +298,7 @@ def test_hybrid_prefix_aligned_recovery_across_processes(mode, tmp_path):
     seed, salt = harness.sub_seed("hybrid-tier", mode), 21
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
     tier = _start_tier(sock, lay, 8, mode, 2, dump, role="tier-native", extra=("8", "2", str(G * pb)))
-    try:
+    with _serving(tier):
         r = subprocess.run([sys.executable, "-u", ROLES, "store-hybrid", sock, *_dims(lay), str(NB), str(n), str(seed),
                             str(salt), str(G), str(pb), str(npages), str(page_a)],
                            capture_output=True, text=True, timeout=120)
@@ -294,8 +317,7 @@ def test_hybrid_prefix_aligned_recovery_across_processes(mode, tmp_path):
         assert kvx.kv_tier_load_prefix(c.fileno(), cB, btB, salt, other, state=sB, state_page=page_b) == 0
         assert kvx.kv_tier_load_prefix(c.fileno(), cB, btB, salt, other) == 3 * lay.C
         c.close()
-    finally:
-        _finish_native(tier)
+    _finish_native(tier)
     assert hit == 5 * lay.C
     A = host_cache(lay, NB, seed, "raw")
     btA = harness.block_table(seed + 1, NB, lay.nblk(n))

@@ -62,6 +62,7 @@ def parse():
     ap.add_argument("--state-only", action="store_true",
                     help="only measure recurrent-state snapshots and print its JSON object (run by the main bench)")
     ap.add_argument("--no-index", action="store_true", help="skip the pool-index measurement")
+    ap.add_argument("--no-session", action="store_true", help="skip the six-turn session measurement")
     ap.add_argument("--no-tier", action="store_true", help="skip the cross-process (tier) measurement")
     ap.add_argument("--tier-only", action="store_true",
                     help="only measure store/restore between processes through a tier (run by the main bench)")
@@ -612,6 +613,110 @@ def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
             "round_trip": "bit-exact (sampled chunks 0, 40, 80 and all snapshot pages)" if ok else "FAILED"}, ok
 
 
+def session_leg(np, torch, harness, hg, kvx, reps, bt_a, layout, mode, dev, turns=6, add=2048):
+    """The six-turn session: an initial 131,072-token context, then 2,048 new tokens per turn.
+    Each turn the producer (alternating replicas) runs a seeded 5-50 ms spin and writes its new
+    tokens' KV on its stream, stores only the new chunks, and the host completes them; the other
+    replica drops its blocks, draws a fresh fragmented set and restores the whole prefix."""
+    n0 = 131072
+    nb = reps[0].num_blocks
+    n_final = n0 + add * (turns - 1)
+    pool = kvx.kv_pool_create(layout, -(-n_final // C), mode)
+    seed = harness.sub_seed("bench-session")
+    delays = harness.spin_delays_ms(seed, turns)
+    rng = np.random.default_rng(seed)
+    tables = [np.asarray(bt_a, dtype=np.int32), None]  # replica A holds the initial context
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    n_prev, out, ok = 0, [], True
+    for t in range(turns):
+        prod, cons = t % 2, 1 - t % 2
+        n = n0 + add * t
+        nblk = -(-n // BS)
+        sp = streams[prod]
+        if t > 0:  # append fresh blocks and write the new tokens' KV into them
+            free = np.setdiff1d(np.arange(nb), tables[prod])
+            extra = rng.permutation(free)[:nblk - len(tables[prod])].astype(np.int32)
+            tables[prod] = np.concatenate([tables[prod], extra])
+            fresh = torch.empty((L, len(extra), 2, H, BS, D), dtype=torch.int16, device=dev)
+            hg.fill_values(fresh, t << 40, seed, "n01", E, sp)
+            hg.spin(float(delays[t]), sp)
+            with torch.cuda.stream(sp):
+                reps[prod].t[:, torch.from_numpy(extra.astype(np.int64)).to(dev)] = fresh
+        else:
+            hg.spin(float(delays[t]), sp)
+        c0 = n_prev // C
+        bt_new = torch.from_numpy(tables[prod][c0 * (C // BS):nblk]).to(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(sp)
+        kvx.kv_store(reps[prod].cache, bt_new, n - c0 * C, pool, np.arange(c0, -(-n // C)), sp)
+        e1.record(sp)
+        sp.synchronize()  # host completion before the other replica reads the pool
+        tables[cons] = rng.permutation(nb)[:nblk].astype(np.int32)
+        tc = torch.from_numpy(tables[cons]).to(dev)
+        sc = streams[cons]
+        sc.synchronize()
+        w0 = time.perf_counter()
+        kvx.kv_load(reps[cons].cache, tc, n, pool, np.arange(-(-n // C)), sc)
+        sc.synchronize()
+        restore = time.perf_counter() - w0
+        tp = torch.from_numpy(tables[prod].astype(np.int64)).to(dev)
+        tcl = tc.long()
+        for k in range(0, nblk, 512):
+            ok = ok and bool(torch.equal(reps[cons].t[:, tcl[k:k + 512]], reps[prod].t[:, tp[k:k + 512]]))
+        out.append({"turn": t, "prefix_tokens": n, "stored_chunks": -(-n // C) - c0,
+                    "store_s": round(e0.elapsed_time(e1) / 1e3, 4), "restore_s": round(restore, 4),
+                    "restore_GBps": round(n * TOKEN_BYTES / restore / 1e9, 3)})
+        n_prev = n
+    ok = ok and kvx.kv_pool_async_error(pool) == 0
+    kvx.kv_pool_destroy(pool)
+    return {"workload": "six-turn session of the 27B-class layout: 131,072 tokens, then 2,048 new tokens per turn; "
+                        "alternating producers store only their new chunks after a seeded 5-50 ms spin and their own "
+                        "fill; the other replica restores the whole prefix into a fresh fragmented block set",
+            "turns": out, "restore_s_median": round(statistics.median(x["restore_s"] for x in out), 4),
+            "verified": "every restored block equals the producer's (all turns)" if ok else "FAILED"}, ok
+
+
+def hbm_copy_achievable(torch, dev, nbytes=4 << 30, reps=5):
+    """Achievable HBM rate of a plain device-to-device copy (read + write bytes per second)."""
+    x = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        y.copy_(x)
+    e1.record()
+    e1.synchronize()
+    return round(2 * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9, 1)
+
+
+def env_record(torch, info):
+    def read(path):
+        try:
+            with open(path) as f:
+                return f.read().strip()
+        except OSError:
+            return None
+    cpu = None
+    for line in (read("/proc/cpuinfo") or "").splitlines():
+        if line.startswith("model name"):
+            cpu = line.split(":", 1)[1].strip()
+            break
+    mems = None
+    for line in (read("/proc/self/status") or "").splitlines():
+        if line.startswith("Mems_allowed_list"):
+            mems = line.split(":", 1)[1].strip()
+    return {"rocm": read("/opt/rocm/.info/version"), "torch": torch.__version__, "hip": torch.version.hip,
+            "gpu": torch.cuda.get_device_properties(0).name, "cpu": cpu, "cpu_count": os.cpu_count(),
+            "cpus_allowed": len(os.sched_getaffinity(0)), "numa_nodes_allowed": mems,
+            "HSA_ENABLE_SDMA": os.environ.get("HSA_ENABLE_SDMA", "unset (runtime default: DMA engines on)"),
+            "GPU_MAX_HW_QUEUES": os.environ.get("GPU_MAX_HW_QUEUES"),
+            "pool": {k: info[k] for k in ("mode", "host_kind", "staging_slots", "chunks_per_batch", "side_streams",
+                                          "staging_contiguous", "is_pinned")}}
+
+
 def cpu_baseline(np, oracle, n_chunks=64):
     """The oracle timed on host cores: store + load of a bounded sample of the workload."""
     rng = np.random.default_rng(2609)
@@ -861,8 +966,17 @@ def main():
             log(f"[bench] {other_mode}: store {zc['store_GBps']} GB/s, load {zc['load_GBps']} GB/s")
     alloc_s = info["alloc_seconds"]
     staging_contig = info["staging_contiguous"]
+    env = env_record(torch, info)
     kvx.kv_pool_destroy(pool)
+    session = None
+    if not args.no_session:
+        session, ok_s = session_leg(np, torch, harness, hg, kvx, [rep_a, rep_b], bt_a, layout, args.mode, dev)
+        ok = ok and ok_s
+        log(f"[bench] session restores (s): {[x['restore_s'] for x in session['turns']]}; {session['verified']}")
     del rep_a, rep_b, t_a, t_b
+    torch.cuda.empty_cache()
+    hbm_copy = hbm_copy_achievable(torch, dev)
+    log(f"[bench] plain device-to-device copy: {hbm_copy} GB/s")
     torch.cuda.empty_cache()
 
     restore_256k = None
@@ -918,6 +1032,9 @@ def main():
 
     store_gbps = N / statistics.median(store_s) / 1e9
     load_gbps = N / statistics.median(load_s) / 1e9
+    spread = {"store_GBps_min_max": [round(N / max(store_s) / 1e9, 3), round(N / min(store_s) / 1e9, 3)],
+              "load_GBps_min_max": [round(N / max(load_s) / 1e9, 3), round(N / min(load_s) / 1e9, 3)],
+              "restore_s_128k_min_max": [round(min(restore), 4), round(max(restore), 4)]}
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 3), "higher_is_better": True,
@@ -931,6 +1048,10 @@ def main():
         "restore_s_128k": round(restore_128k, 4),
         "restore_s_256k": None if restore_256k is None else round(restore_256k, 4),
         "restore_s_by_prefix_tokens": restore_by_len,
+        "spread": spread,
+        "session": session,
+        "hbm_copy_achievable_GBps": hbm_copy,
+        "env": env,
         "link": {"peak_d2h_GBps": round(peak["d2h"], 3), "peak_h2d_GBps": round(peak["h2d"], 3),
                  "store_frac_of_peak": round(store_gbps / peak["d2h"], 4),
                  "load_frac_of_peak": round(load_gbps / peak["h2d"], 4),

@@ -177,3 +177,24 @@ def test_hybrid_session_aligned_recovery(mode):
     assert np.array_equal(got_S[:, page_B], SA[:, snap_page_after[k - 1]])
     assert not got_S[:, [p for p in range(npages) if p != page_B]].any()
     kvx.kv_pool_destroy(pool)
+
+
+def test_state_area_options_are_validated():
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_pool_create(TINY.kv, 2, "staged", num_state_slots=2, state_slot_bytes=0)
+    assert e.value.status == kvx.KV_EINVAL
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_pool_create(TINY.kv, 2, "staged", num_state_slots=0, state_slot_bytes=4096)
+    assert e.value.status == kvx.KV_EINVAL
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_pool_create(TINY.kv, 2, "staged", num_state_slots=2, state_slot_bytes=4104)
+    assert e.value.status == kvx.KV_EUNSUPPORTED
+    pool = kvx.kv_pool_create(TINY.kv, 3, "zero_copy", num_state_slots=2, state_slot_bytes=4096)
+    info = kvx.kv_pool_get_info(pool)
+    assert info["num_state_slots"] == 2 and info["state_slot_bytes"] == 4096
+    # The state area follows the chunk slots in the same pinned region, 4 KiB aligned.
+    assert info["state_host_base"] >= info["host_base"] + info["pool_bytes"]
+    assert info["state_host_base"] % 4096 == 0
+    assert kvx.kv_pool_state_slot(pool, 1) == info["state_host_base"] + 4096
+    assert kvx.kv_pool_state_slot(pool, 2) == 0
+    kvx.kv_pool_destroy(pool)

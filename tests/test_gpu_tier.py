@@ -328,3 +328,32 @@ def test_hybrid_prefix_aligned_recovery_across_processes(mode, tmp_path):
     pages_A = state_pages(seed, G, npages, pb)
     assert np.array_equal(got_S[:, page_b], pages_A[:, page_a])
     assert not got_S[:, [p for p in range(npages) if p != page_b]].any()
+
+
+def test_two_replicas_store_at_the_same_time(tmp_path):
+    """Two replica processes store different prompts through one tier concurrently (one native
+    thread each, requests served one at a time); a third replica then hits both prompts whole."""
+    lay = TINY
+    n = 3 * lay.C
+    NB = lay.nblk(n) + 4
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    tier = _start_tier(sock, lay, 8, "staged", 3, dump, role="tier-native", extra=("8",))
+    with _serving(tier):
+        procs = [subprocess.Popen([sys.executable, "-u", ROLES, "store-prefix", sock, *_dims(lay), str(NB), str(n),
+                                   str(seed), "9"], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+                 for seed in (303, 404)]
+        outs = [p.communicate(timeout=120)[0] for p in procs]
+        assert all(p.returncode == 0 and "STORED 3" in o for p, o in zip(procs, outs)), outs
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
+        cB = kvx.Cache(dB, lay.kv, NB)
+        bt = np.arange(lay.nblk(n), dtype=np.int32)
+        torch.cuda.synchronize()
+        c = _connect(sock)
+        for seed in (303, 404):
+            assert kvx.kv_tier_load_prefix(c.fileno(), cB, bt, 9, harness.prompt_tokens(seed, n)) == n
+            got = dB.cpu().numpy().view(np.uint16)
+            A = host_cache(lay, NB, seed, "raw")
+            btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+            assert np.array_equal(got[:, bt], A[:, btA]), f"prompt {seed} restored wrong bytes"
+        c.close()
+    _finish_native(tier)

@@ -145,3 +145,38 @@ def test_index_argument_errors():
         kvx.kv_index_commit(x, slots, new)                                   # no longer pinned
     with pytest.raises(kvx.KvError):
         kvx.kv_index_reserve_state(x, int(slots[0]))                         # not pinned
+
+
+def test_index_under_concurrent_threads():
+    """Four threads store and look up their own prompts on one index at the same time (the calls
+    release the GIL): every thread's final lookups hit its whole prompt and no pin is left."""
+    import threading
+    C, per = 8, 6
+    x = kvx.kv_index_create(C, 4 * per)
+    rng = np.random.default_rng(17)
+    prompts = [rng.integers(0, 50000, size=per * C).astype(np.int32) for _ in range(4)]
+    errors = []
+
+    def worker(k):
+        try:
+            for _ in range(300):
+                slots, new = kvx.kv_index_reserve(x, k, prompts[k])
+                kvx.kv_index_commit(x, slots, new, True)
+                r = kvx.kv_index_lookup(x, k, prompts[k], pin=True)
+                kvx.kv_index_unpin(x, r["slots"])
+                if r["hit_chunks"] != per:
+                    errors.append((k, r["hit_chunks"]))
+        except Exception as e:  # surfaced below
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors[:5]
+    st = kvx.kv_index_get_stats(x)
+    assert st["entries"] == 4 * per and st["pending"] == 0 and st["evictions"] == 0
+    for k in range(4):
+        assert kvx.kv_index_lookup(x, k, prompts[k])["hit_chunks"] == per
+    kvx.kv_index_destroy(x)

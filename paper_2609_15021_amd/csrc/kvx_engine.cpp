@@ -395,13 +395,25 @@ kv_status transfer_state(kv_pool *p, const kv_state *st, const int64_t *pages, i
     return staged_pipeline(p, nbatches, runs_of, kernels, stream, dir);
 }
 
-// Record the pool's last use on `stream` (one event per stream seen).
+// Record the pool's last use on `stream` (one event per stream with work in flight).  Entries of
+// other streams whose recorded work has completed are dropped, so callers that use many
+// short-lived streams do not grow the list.
 kv_status mark_use(kv_pool *p, hipStream_t stream) {
     for (auto &use : p->last_use)
         if (use.first == stream) {
             KVX_HIP(hipEventRecord(use.second, stream));
             return KV_OK;
         }
+    for (size_t i = 0; i < p->last_use.size();) {
+        if (hipEventQuery(p->last_use[i].second) == hipSuccess) {
+            KVX_HIP(hipEventDestroy(p->last_use[i].second));
+            p->last_use[i] = p->last_use.back();
+            p->last_use.pop_back();
+        } else {
+            ++i;
+        }
+    }
+    (void)hipGetLastError();  // a not-ready query leaves no error behind
     hipEvent_t e = nullptr;
     kv_status st = make_event(&e, false);
     if (st != KV_OK)

@@ -76,3 +76,27 @@ def test_two_threads_share_one_pool(mode):
     want = oracle_pool(lay, A, bt, n, np.arange(16), 16, 0)
     assert np.array_equal(view, want)
     kvx.kv_pool_destroy(pool)
+
+
+def test_many_short_lived_streams():
+    """A store on each of 40 fresh streams: every one is ordered and the pool stays usable; streams
+    whose work completed do not accumulate in the pool."""
+    lay, NB, n = TINY, 512, 1024
+    seed = harness.sub_seed("streams")
+    A = host_cache(lay, NB, seed, "raw")
+    bt = harness.block_table(seed + 1, NB, lay.nblk(n))
+    pool = kvx.kv_pool_create(lay.kv, lay.nc(n), "staged", staging_slots=2, chunks_per_batch=2)
+    view = kvx.pool_view(pool)
+    dA = to_device(A)
+    cache = kvx.Cache(dA, lay.kv, NB)
+    tb = bt_tensor(bt)
+    torch.cuda.synchronize()
+    for _ in range(40):
+        s = torch.cuda.Stream()
+        view[:] = 0
+        kvx.kv_store(cache, tb, n, pool, np.arange(lay.nc(n)), s)
+        s.synchronize()
+        del s
+    want = oracle_pool(lay, A, bt, n, np.arange(lay.nc(n)), lay.nc(n), 0)
+    assert np.array_equal(view, want)
+    kvx.kv_pool_destroy(pool)

@@ -938,17 +938,23 @@ def main():
         restore.append(time.perf_counter() - w0)
     restore_128k = statistics.median(restore)
     # The paper's shorter prompts (Sec. 4.2: 8k to 256k tokens): prefixes of the same stored chunks.
-    restore_by_len = {}
+    # Stores of the same prefixes rewrite the same bytes into the same slots.
+    restore_by_len, store_by_len = {}, {}
     for m in (8192, 32768, 65536):
-        ts = []
+        ts, tw = [], []
         for _ in range(3):
+            w0 = time.perf_counter()
+            kvx.kv_store(rep_a.cache, t_a, m, pool, ids[:-(-m // C)], s)
+            s.synchronize()
+            tw.append(time.perf_counter() - w0)
             w0 = time.perf_counter()
             kvx.kv_load(rep_b.cache, t_b, m, pool, ids[:-(-m // C)], s)
             s.synchronize()
             ts.append(time.perf_counter() - w0)
         restore_by_len[str(m)] = round(statistics.median(ts), 4)
+        store_by_len[str(m)] = round(m * TOKEN_BYTES / statistics.median(tw) / 1e9, 3)
     restore_by_len[str(n)] = round(restore_128k, 4)
-    log(f"[bench] restore seconds by prefix length: {restore_by_len}")
+    log(f"[bench] restore seconds by prefix length: {restore_by_len}; store GB/s (host wall clock): {store_by_len}")
 
     zc = None
     if not args.no_zero_copy_compare:
@@ -1048,6 +1054,7 @@ def main():
         "restore_s_128k": round(restore_128k, 4),
         "restore_s_256k": None if restore_256k is None else round(restore_256k, 4),
         "restore_s_by_prefix_tokens": restore_by_len,
+        "store_GBps_by_prefix_tokens": store_by_len,
         "spread": spread,
         "session": session,
         "hbm_copy_achievable_GBps": hbm_copy,

@@ -987,6 +987,7 @@ def main():
 
     restore_256k = None
     parity_256k = None
+    alloc_s_256k = None
     if not args.no_256k:
         n2, nb2 = 262336, 20480  # 1,024 full chunks + a 192-token partial chunk; 80 GiB allocations
         nc2, nblk2 = -(-n2 // C), -(-n2 // BS)
@@ -998,6 +999,7 @@ def main():
         ta, tb = torch.from_numpy(ba).to(dev), torch.from_numpy(bb).to(dev)
         ids2 = harness.chunk_ids(nc2, nc2)
         pool2 = kvx.kv_pool_create(layout, nc2, args.mode, staging_slots=3 if args.mode == "staged" else 0)
+        alloc_s_256k = kvx.kv_pool_get_info(pool2)["alloc_seconds"]
         torch.cuda.synchronize()  # fills ran on the default stream; s is non-blocking
         kvx.kv_store(ra.cache, ta, n2, pool2, ids2, s)
         s.synchronize()
@@ -1066,6 +1068,7 @@ def main():
         "roofline": roof,
         "zero_copy_compare": zc,
         "pool_alloc_s": round(alloc_s, 4),
+        "pool_alloc_s_256k": None if alloc_s_256k is None else round(alloc_s_256k, 4),
         "staging_contiguous": bool(staging_contig),
         "parity": parity_msg if ok else f"FAILED: {parity_msg}",
         "parity_256k": parity_256k,

@@ -149,3 +149,14 @@ def test_random_sequences_keep_invariants():
         assert m.commit(slots, new, ok) == 0
     _invariants(m)
     assert all(e["pins"] == 0 for e in m.slot.values())
+
+
+def test_new_entries_take_the_lowest_free_slot():
+    m = PoolIndexModel(2, 6)
+    a = _store(m, 0, [1, 1, 2, 2, 3, 3])          # 3 chunks -> slots 0, 1, 2
+    assert a == [0, 1, 2]
+    st, slots, new = m.reserve(0, [7, 7, 8, 8], 4)  # 2 chunks -> 3, 4; then abort them
+    assert slots == [3, 4]
+    m.commit(slots, new, False)
+    b = _store(m, 0, [9, 9], 2)                    # the freed slot 3 is the lowest again
+    assert b == [3]

@@ -6,6 +6,7 @@ its prefix through the tier; replica B (this test) loads it into a fresh fragmen
 The pool bytes (dumped by the tier) and B's cache are compared with the oracle.
 """
 import contextlib
+import gc
 import os
 import socket
 import subprocess
@@ -28,6 +29,7 @@ def _fresh_segments():
     """Buffers shared with the tier must be their own allocations under 2 GiB: release the caching
     allocator's free segments first (earlier tests leave huge ones that small tensors would be
     carved from, and kv_ipc_export rightly refuses to share those)."""
+    gc.collect()  # tensors held only by reference cycles (e.g. a caught exception's frames) go first
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     yield
@@ -166,11 +168,17 @@ def test_ipc_export_refuses_allocations_of_2_gib():
     t = torch.empty(2 << 30, dtype=torch.uint8, device=DEV)
     with pytest.raises(kvx.KvError) as e:
         kvx.kv_ipc_export(t)
-    assert e.value.status == kvx.KV_EUNSUPPORTED
+    status = e.value.status
+    # The caught exception's traceback holds the frames that reference t (a reference cycle):
+    # drop it and collect, or the 2 GiB segment outlives the test and later small tensors are
+    # carved from it.
+    del e
+    assert status == kvx.KV_EUNSUPPORTED
     small = torch.empty(1 << 20, dtype=torch.uint8, device=DEV)
     buf = kvx.kv_ipc_export(small[4096:])
     assert buf.allocation_bytes < (2 << 30) and buf.offset >= 4096
-    del t
+    del t, small
+    gc.collect()
     torch.cuda.empty_cache()
 
 

@@ -717,6 +717,40 @@ def env_record(torch, info):
                                           "staging_contiguous", "is_pinned")}}
 
 
+def concurrent_leg(torch, kvx, rep_a, rep_b, t_a, t_b, n, ids, pool, reps=3):
+    """A store and a load in flight together on two streams (one replica storing while another
+    restores), each half of the prefix.  Returns per-direction and aggregate GB/s (median of
+    `reps`; wall clock from the first enqueue until both streams completed)."""
+    half_c = len(ids) // 2
+    m = half_c * C
+    nb = m // BS
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    walls, st, ld = [], [], []
+    for _ in range(reps + 1):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        w0 = time.perf_counter()
+        e[0].record(s1)
+        e[2].record(s2)
+        kvx.kv_store(rep_a.cache, t_a, m, pool, ids[:half_c], s1)
+        kvx.kv_load(rep_b.cache, t_b[nb:], n - m, pool, ids[half_c:], s2)
+        e[1].record(s1)
+        e[3].record(s2)
+        s1.synchronize()
+        s2.synchronize()
+        walls.append(time.perf_counter() - w0)
+        st.append(e[0].elapsed_time(e[1]) / 1e3)
+        ld.append(e[2].elapsed_time(e[3]) / 1e3)
+    walls, st, ld = walls[1:], st[1:], ld[1:]  # the first pass is a warm-up
+    sb, lb = m * TOKEN_BYTES, (n - m) * TOKEN_BYTES
+    return {"bytes_per_direction": sb, "seconds": round(statistics.median(walls), 4),
+            "aggregate_GBps": round((sb + lb) / statistics.median(walls) / 1e9, 2),
+            "store_GBps": round(sb / statistics.median(st) / 1e9, 2),
+            "load_GBps": round(lb / statistics.median(ld) / 1e9, 2),
+            "workload": f"store of tokens [0, {m:,}) from replica A and load of tokens [{m:,}, {n:,}) into "
+                        "replica B, enqueued together on two streams, disjoint slots"}
+
+
 def cpu_baseline(np, oracle, n_chunks=64):
     """The oracle timed on host cores: store + load of a bounded sample of the workload."""
     rng = np.random.default_rng(2609)
@@ -956,6 +990,13 @@ def main():
     restore_by_len[str(n)] = round(restore_128k, 4)
     log(f"[bench] restore seconds by prefix length: {restore_by_len}; store GB/s (host wall clock): {store_by_len}")
 
+    # Two replicas at once: replica A stores the first half of the prefix into slots 0..nc/2-1 on
+    # one stream while replica B loads the second half from slots nc/2..nc-1 on another.  The
+    # calls touch disjoint slots, and the store rewrites the bytes those slots hold.
+    both = concurrent_leg(torch, kvx, rep_a, rep_b, t_a, t_b, n, ids, pool)
+    log(f"[bench] store and load at once ({both['bytes_per_direction'] / 2**30:.0f} GiB each): "
+        f"{both['aggregate_GBps']} GB/s in total (store {both['store_GBps']}, load {both['load_GBps']} GB/s)")
+
     zc = None
     if not args.no_zero_copy_compare:
         other_mode = "zero_copy" if args.mode == "staged" else "staged"
@@ -1066,6 +1107,7 @@ def main():
                  "load_frac_of_peak": round(load_gbps / peak["h2d"], 4),
                  "peak_method": "median of 10 pinned hipMemcpyAsync of 1 GiB on the pool's own memory"},
         "roofline": roof,
+        "concurrent_store_load": both,
         "zero_copy_compare": zc,
         "pool_alloc_s": round(alloc_s, 4),
         "pool_alloc_s_256k": None if alloc_s_256k is None else round(alloc_s_256k, 4),

@@ -9,6 +9,7 @@ import pytest
 import torch
 
 import harness
+from harness import gpu as hg
 from paper_2609_15021_amd import kvx
 from tests.gpu_support import (DEV, TINY, Layout, bt_tensor, device_cache, first_mismatch, host_cache,
                                oracle_pool, oracle_unpack_into, to_device, to_host)
@@ -206,6 +207,55 @@ def test_out_of_range_block_is_flagged_and_skipped(mode):
     want = oracle_pool(lay, spare, bt0, n, [0, 1], 2, POOL_SENT)
     assert np.array_equal(view, want), first_mismatch(view, want)
     assert kvx.kv_pool_async_error(pool, clear=True) == kvx.KV_ASYNC_BAD_BLOCK
+    assert kvx.kv_pool_async_error(pool) == 0
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_concurrent_store_and_load_on_two_streams(mode):
+    """Two replicas use one pool at once: one stores prefix Q into slots Y on stream s1 while
+    another loads prefix P from slots X on stream s2 (the caller orders nothing between them:
+    the two calls touch disjoint slots).  With a 2-slot ring of 1-chunk batches, the store's and
+    the load's batches take turns in the shared staging ring many times while both are in
+    flight; s1 starts behind a 20 ms spin so that the load runs first and the two interleave.
+    Pool and caches equal the oracle's bytes."""
+    lay = TINY
+    NB, n = 512, 5 * lay.C + 77
+    nc, nblk = lay.nc(n), lay.nblk(n)
+    seed = harness.sub_seed("parity", "two-streams", mode)
+    A = host_cache(lay, NB, seed, "raw")
+    Q = host_cache(lay, NB, seed + 10, "raw")
+    btA, btQ, btB = (harness.block_table(seed + k, NB, nblk) for k in (1, 2, 3))
+    num_slots = 2 * nc + 1
+    ids = harness.chunk_ids(2 * nc, num_slots, seed + 4)
+    idsX, idsY = ids[:nc], ids[nc:]
+    pool = kvx.kv_pool_create(lay.kv, num_slots, mode, staging_slots=2, chunks_per_batch=1)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    dA, dQ = to_device(A), to_device(Q)
+    dB = device_cache(lay, NB, fill=CACHE_SENT)
+    cA, cQ, cB = (kvx.Cache(d, lay.kv, NB) for d in (dA, dQ, dB))
+    tA, tQ, tB = bt_tensor(btA), bt_tensor(btQ), bt_tensor(btB)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    kvx.kv_store(cA, tA, n, pool, idsX, s2)     # prefix P in slots X
+    s2.synchronize()
+    hg.spin(20.0, s1)
+    for _ in range(3):                          # the same bytes each time
+        kvx.kv_store(cQ, tQ, n, pool, idsY, s1)
+        kvx.kv_load(cB, tB, n, pool, idsX, s2)
+    s1.synchronize()
+    s2.synchronize()
+    want_pool = oracle_pool(lay, A, btA, n, idsX, num_slots, POOL_SENT)
+    qpool = oracle_pool(lay, Q, btQ, n, idsY, num_slots, POOL_SENT)
+    for i in idsY:
+        want_pool[i * lay.slot_bytes:(i + 1) * lay.slot_bytes] = qpool[i * lay.slot_bytes:(i + 1) * lay.slot_bytes]
+    assert np.array_equal(view, want_pool), "pool: " + first_mismatch(view, want_pool)
+    B0 = np.full(A.shape, 0, dtype=A.dtype)
+    B0.view(np.uint8)[:] = CACHE_SENT
+    want_B = oracle_unpack_into(lay, B0, btB, n, want_pool, idsX)
+    got_B = to_host(dB, A)
+    assert np.array_equal(got_B, want_B), "cache B: " + first_mismatch(got_B, want_B)
     assert kvx.kv_pool_async_error(pool) == 0
     kvx.kv_pool_destroy(pool)
 

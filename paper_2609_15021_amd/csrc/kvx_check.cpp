@@ -229,12 +229,16 @@ const char *kv_version(void) { return "kvx 0.1.0 (gfx950)"; }
 
 kv_status kv_check(const kv_cache *cache, const kv_layout *pool_layout, int64_t pool_slots, int64_t n_tokens,
                    const int64_t *chunk_ids, int for_store) {
-    return kvx::check_request(cache, pool_layout, pool_slots, n_tokens, chunk_ids, for_store);
+    return kvx::guarded([&]() -> kv_status {
+        return kvx::check_request(cache, pool_layout, pool_slots, n_tokens, chunk_ids, for_store);
+    });
 }
 
 kv_status kv_check_state(const kv_state *state, int64_t pool_state_slot_bytes, int64_t pool_state_slots, int64_t n,
                          const int64_t *pages, const int64_t *slot_ids, int for_store) {
-    return kvx::check_state_request(state, pool_state_slot_bytes, pool_state_slots, n, pages, slot_ids, for_store);
+    return kvx::guarded([&]() -> kv_status {
+        return kvx::check_state_request(state, pool_state_slot_bytes, pool_state_slots, n, pages, slot_ids, for_store);
+    });
 }
 
 }  // extern "C"

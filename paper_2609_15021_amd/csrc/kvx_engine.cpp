@@ -473,190 +473,202 @@ kv_status run_state(const kv_state *state, const int64_t *pages, int64_t n, kv_p
 extern "C" {
 
 kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_pool_options *opts, kv_pool **out) {
-    if (!layout || !opts || !out)
-        return kvx::fail(KV_EINVAL, "layout, opts and out must not be NULL");
-    *out = nullptr;
-    kv_status st = kvx::check_layout(*layout);
-    if (st != KV_OK)
-        return st;
-    if (num_slots <= 0 || num_slots > INT32_MAX)
-        return kvx::fail(KV_EINVAL, "num_slots must be in [1, 2^31-1] (got %lld)", static_cast<long long>(num_slots));
-    if (opts->mode != KV_MODE_ZERO_COPY && opts->mode != KV_MODE_STAGED)
-        return kvx::fail(KV_EINVAL, "opts->mode must be KV_MODE_ZERO_COPY or KV_MODE_STAGED (got %u)", opts->mode);
-    if (opts->host_kind != KV_HOST_COHERENT && opts->host_kind != KV_HOST_NONCOHERENT)
-        return kvx::fail(KV_EINVAL, "unknown host_kind %u", opts->host_kind);
-    // chunks_per_batch applies to the mode chosen at creation; the other mode keeps its default.
-    if (opts->chunks_per_batch < 0 || opts->chunks_per_batch > kvx::kMaxLaunchChunks)
-        return kvx::fail(KV_EINVAL, "chunks_per_batch must be in [1, %d] (got %d)", kvx::kMaxLaunchChunks,
-                         opts->chunks_per_batch);
-    const bool staged = opts->mode == KV_MODE_STAGED;
-    const int cpb = (staged && opts->chunks_per_batch) ? opts->chunks_per_batch : kDefaultChunksPerBatch;
-    const int zc_chunks = (!staged && opts->chunks_per_batch) ? opts->chunks_per_batch : kvx::kMaxLaunchChunks;
-    const bool want_staging = opts->mode == KV_MODE_STAGED || opts->staging_slots > 0;
-    const int K = opts->staging_slots ? opts->staging_slots : kDefaultStagingSlots;
-    if (want_staging && (K < 2 || K > 64))
-        return kvx::fail(KV_EINVAL, "staging_slots must be in [2, 64] (got %d)", K);
-    const int S = opts->side_streams ? opts->side_streams : kDefaultSideStreams;
-    if (want_staging && (S < 1 || S > 8))
-        return kvx::fail(KV_EINVAL, "side_streams must be in [1, 8] (got %d)", S);
-    if (opts->num_state_slots < 0 || opts->state_slot_bytes < 0 ||
-        (opts->num_state_slots > 0) != (opts->state_slot_bytes > 0))
-        return kvx::fail(KV_EINVAL, "num_state_slots (%lld) and state_slot_bytes (%lld) must both be 0 or both > 0",
-                         static_cast<long long>(opts->num_state_slots), static_cast<long long>(opts->state_slot_bytes));
-    if (opts->state_slot_bytes % 16 != 0)
-        return kvx::fail(KV_EUNSUPPORTED, "state_slot_bytes %lld is not a multiple of 16",
-                         static_cast<long long>(opts->state_slot_bytes));
+    return kvx::guarded([&]() -> kv_status {
+        if (!layout || !opts || !out)
+            return kvx::fail(KV_EINVAL, "layout, opts and out must not be NULL");
+        *out = nullptr;
+        kv_status st = kvx::check_layout(*layout);
+        if (st != KV_OK)
+            return st;
+        if (num_slots <= 0 || num_slots > INT32_MAX)
+            return kvx::fail(KV_EINVAL, "num_slots must be in [1, 2^31-1] (got %lld)", static_cast<long long>(num_slots));
+        if (opts->mode != KV_MODE_ZERO_COPY && opts->mode != KV_MODE_STAGED)
+            return kvx::fail(KV_EINVAL, "opts->mode must be KV_MODE_ZERO_COPY or KV_MODE_STAGED (got %u)", opts->mode);
+        if (opts->host_kind != KV_HOST_COHERENT && opts->host_kind != KV_HOST_NONCOHERENT)
+            return kvx::fail(KV_EINVAL, "unknown host_kind %u", opts->host_kind);
+        // chunks_per_batch applies to the mode chosen at creation; the other mode keeps its default.
+        if (opts->chunks_per_batch < 0 || opts->chunks_per_batch > kvx::kMaxLaunchChunks)
+            return kvx::fail(KV_EINVAL, "chunks_per_batch must be in [1, %d] (got %d)", kvx::kMaxLaunchChunks,
+                             opts->chunks_per_batch);
+        const bool staged = opts->mode == KV_MODE_STAGED;
+        const int cpb = (staged && opts->chunks_per_batch) ? opts->chunks_per_batch : kDefaultChunksPerBatch;
+        const int zc_chunks = (!staged && opts->chunks_per_batch) ? opts->chunks_per_batch : kvx::kMaxLaunchChunks;
+        const bool want_staging = opts->mode == KV_MODE_STAGED || opts->staging_slots > 0;
+        const int K = opts->staging_slots ? opts->staging_slots : kDefaultStagingSlots;
+        if (want_staging && (K < 2 || K > 64))
+            return kvx::fail(KV_EINVAL, "staging_slots must be in [2, 64] (got %d)", K);
+        const int S = opts->side_streams ? opts->side_streams : kDefaultSideStreams;
+        if (want_staging && (S < 1 || S > 8))
+            return kvx::fail(KV_EINVAL, "side_streams must be in [1, 8] (got %d)", S);
+        if (opts->num_state_slots < 0 || opts->state_slot_bytes < 0 ||
+            (opts->num_state_slots > 0) != (opts->state_slot_bytes > 0))
+            return kvx::fail(KV_EINVAL, "num_state_slots (%lld) and state_slot_bytes (%lld) must both be 0 or both > 0",
+                             static_cast<long long>(opts->num_state_slots), static_cast<long long>(opts->state_slot_bytes));
+        if (opts->state_slot_bytes % 16 != 0)
+            return kvx::fail(KV_EUNSUPPORTED, "state_slot_bytes %lld is not a multiple of 16",
+                             static_cast<long long>(opts->state_slot_bytes));
 
-    kv_pool *p = new kv_pool();
-    p->layout = *layout;
-    p->geo = kvx::geometry(*layout, 0);
-    p->num_slots = num_slots;
-    if (p->geo.slot_bytes > INT64_MAX / num_slots) {
-        delete p;
-        return kvx::fail(KV_EINVAL, "pool size overflows 64 bits");
-    }
-    p->pool_bytes = num_slots * p->geo.slot_bytes;
-    // The state-snapshot area follows the chunk slots in the same region, 4 KiB aligned.
-    p->num_state_slots = opts->num_state_slots;
-    p->state_slot_bytes = opts->state_slot_bytes;
-    p->state_offset = (p->pool_bytes + 4095) / 4096 * 4096;
-    if (p->num_state_slots > 0 && p->state_slot_bytes > (INT64_MAX - p->state_offset) / p->num_state_slots) {
-        delete p;
-        return kvx::fail(KV_EINVAL, "pool size with the state area overflows 64 bits");
-    }
-    const int64_t region_bytes =
-        p->num_state_slots > 0 ? p->state_offset + p->num_state_slots * p->state_slot_bytes : p->pool_bytes;
-    p->mode = opts->mode;
-    p->host_kind = opts->host_kind;
-    p->profile = opts->profile != 0;
-    p->zc_chunks = zc_chunks;
-
-    // On failure: free what was made, keeping the original error text.
-    auto bail = [&](kv_status code) {
-        const std::string msg = kv_last_error();
-        release(p);
-        kvx::set_last_error(msg);
-        return code;
-    };
-
-    hipError_t e = hipGetDevice(&p->device);
-    if (e != hipSuccess)
-        return bail(kvx::hip_fail(e, "hipGetDevice", __FILE__, __LINE__));
-
-    // One pinned, mapped region of exactly region_bytes (Sec. 3.3: no rounding allocator,
-    // and never a silent fallback to pageable memory).
-    const unsigned flags = hipHostMallocMapped | hipHostMallocPortable |
-                           (p->host_kind == KV_HOST_COHERENT ? hipHostMallocCoherent : hipHostMallocNonCoherent);
-    const auto t0 = std::chrono::steady_clock::now();
-    void *host = nullptr;
-    e = hipHostMalloc(&host, static_cast<size_t>(region_bytes), flags);
-    const auto t1 = std::chrono::steady_clock::now();
-    if (e != hipSuccess || !host) {
-        (void)hipGetLastError();
-        const long long want = static_cast<long long>(region_bytes);
-        release(p);
-        return kvx::fail(KV_ENOMEM, "pinned allocation of %lld bytes failed (%s); no pageable fallback", want,
-                         hipGetErrorName(e));
-    }
-    p->host_base = static_cast<uint8_t *>(host);
-    p->alloc_seconds = std::chrono::duration<double>(t1 - t0).count();
-
-    hipPointerAttribute_t attr;
-    std::memset(&attr, 0, sizeof(attr));
-    e = hipPointerGetAttributes(&attr, host);
-    if (e != hipSuccess)
-        return bail(kvx::hip_fail(e, "hipPointerGetAttributes(pool)", __FILE__, __LINE__));
-    p->pinned = attr.type == hipMemoryTypeHost;
-    if (!p->pinned)
-        return bail(kvx::fail(KV_ENOMEM, "pool memory is not reported as pinned host memory"));
-    void *dptr = nullptr;
-    e = hipHostGetDevicePointer(&dptr, host, 0);
-    if (e != hipSuccess)
-        return bail(kvx::hip_fail(e, "hipHostGetDevicePointer(pool)", __FILE__, __LINE__));
-    p->dev_base = static_cast<uint8_t *>(dptr);
-
-    e = hipHostMalloc(reinterpret_cast<void **>(&p->err_host), 256, hipHostMallocMapped | hipHostMallocCoherent);
-    if (e != hipSuccess)
-        return bail(kvx::hip_fail(e, "hipHostMalloc(err)", __FILE__, __LINE__));
-    std::memset(p->err_host, 0, 256);
-    e = hipHostGetDevicePointer(reinterpret_cast<void **>(&p->err_dev), p->err_host, 0);
-    if (e != hipSuccess)
-        return bail(kvx::hip_fail(e, "hipHostGetDevicePointer(err)", __FILE__, __LINE__));
-
-    if (want_staging) {
-        p->K = K;
-        p->cpb = cpb;
-        p->S = S;
-        const size_t staging_bytes = static_cast<size_t>(K) * cpb * static_cast<size_t>(p->geo.slot_bytes);
-        // Physically contiguous staging: the DMA engines read and write it, and staging placed in
-        // fragmented (recycled) device memory was measured to slow D2H copies by ~5%.  If the
-        // runtime refuses the flag, plain device memory is used and kv_pool_info reports it.
-        e = hipExtMallocWithFlags(reinterpret_cast<void **>(&p->staging), staging_bytes, hipDeviceMallocContiguous);
-        p->staging_contiguous = e == hipSuccess;
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            e = hipMalloc(reinterpret_cast<void **>(&p->staging), staging_bytes);
+        kv_pool *p = new kv_pool();
+        p->layout = *layout;
+        p->geo = kvx::geometry(*layout, 0);
+        p->num_slots = num_slots;
+        if (p->geo.slot_bytes > INT64_MAX / num_slots) {
+            delete p;
+            return kvx::fail(KV_EINVAL, "pool size overflows 64 bits");
         }
-        if (e != hipSuccess)
-            return bail(kvx::hip_fail(e, "hipMalloc(staging)", __FILE__, __LINE__));
-        for (int s = 0; s < S; ++s) {
-            hipStream_t side = nullptr;
-            // Default priority on purpose: every stream of the library shares one priority.
-            e = hipStreamCreateWithFlags(&side, hipStreamNonBlocking);
+        p->pool_bytes = num_slots * p->geo.slot_bytes;
+        // The state-snapshot area follows the chunk slots in the same region, 4 KiB aligned.
+        p->num_state_slots = opts->num_state_slots;
+        p->state_slot_bytes = opts->state_slot_bytes;
+        p->state_offset = (p->pool_bytes + 4095) / 4096 * 4096;
+        if (p->num_state_slots > 0 && p->state_slot_bytes > (INT64_MAX - p->state_offset) / p->num_state_slots) {
+            delete p;
+            return kvx::fail(KV_EINVAL, "pool size with the state area overflows 64 bits");
+        }
+        const int64_t region_bytes =
+            p->num_state_slots > 0 ? p->state_offset + p->num_state_slots * p->state_slot_bytes : p->pool_bytes;
+        // From here on the pool owns runtime resources: release them if a host container throws.
+        try {
+            p->mode = opts->mode;
+            p->host_kind = opts->host_kind;
+            p->profile = opts->profile != 0;
+            p->zc_chunks = zc_chunks;
+
+            // On failure: free what was made, keeping the original error text.
+            auto bail = [&](kv_status code) {
+                const std::string msg = kv_last_error();
+                release(p);
+                kvx::set_last_error(msg);
+                return code;
+            };
+
+            hipError_t e = hipGetDevice(&p->device);
             if (e != hipSuccess)
-                return bail(kvx::hip_fail(e, "hipStreamCreateWithFlags", __FILE__, __LINE__));
-            p->sides.push_back(side);
-            hipEvent_t j = nullptr;
-            if ((st = make_event(&j, false)) != KV_OK)
-                return bail(st);
-            p->ev_join.push_back(j);
+                return bail(kvx::hip_fail(e, "hipGetDevice", __FILE__, __LINE__));
+
+            // One pinned, mapped region of exactly region_bytes (Sec. 3.3: no rounding allocator,
+            // and never a silent fallback to pageable memory).
+            const unsigned flags = hipHostMallocMapped | hipHostMallocPortable |
+                                   (p->host_kind == KV_HOST_COHERENT ? hipHostMallocCoherent : hipHostMallocNonCoherent);
+            const auto t0 = std::chrono::steady_clock::now();
+            void *host = nullptr;
+            e = hipHostMalloc(&host, static_cast<size_t>(region_bytes), flags);
+            const auto t1 = std::chrono::steady_clock::now();
+            if (e != hipSuccess || !host) {
+                (void)hipGetLastError();
+                const long long want = static_cast<long long>(region_bytes);
+                release(p);
+                return kvx::fail(KV_ENOMEM, "pinned allocation of %lld bytes failed (%s); no pageable fallback", want,
+                                 hipGetErrorName(e));
+            }
+            p->host_base = static_cast<uint8_t *>(host);
+            p->alloc_seconds = std::chrono::duration<double>(t1 - t0).count();
+
+            hipPointerAttribute_t attr;
+            std::memset(&attr, 0, sizeof(attr));
+            e = hipPointerGetAttributes(&attr, host);
+            if (e != hipSuccess)
+                return bail(kvx::hip_fail(e, "hipPointerGetAttributes(pool)", __FILE__, __LINE__));
+            p->pinned = attr.type == hipMemoryTypeHost;
+            if (!p->pinned)
+                return bail(kvx::fail(KV_ENOMEM, "pool memory is not reported as pinned host memory"));
+            void *dptr = nullptr;
+            e = hipHostGetDevicePointer(&dptr, host, 0);
+            if (e != hipSuccess)
+                return bail(kvx::hip_fail(e, "hipHostGetDevicePointer(pool)", __FILE__, __LINE__));
+            p->dev_base = static_cast<uint8_t *>(dptr);
+
+            e = hipHostMalloc(reinterpret_cast<void **>(&p->err_host), 256, hipHostMallocMapped | hipHostMallocCoherent);
+            if (e != hipSuccess)
+                return bail(kvx::hip_fail(e, "hipHostMalloc(err)", __FILE__, __LINE__));
+            std::memset(p->err_host, 0, 256);
+            e = hipHostGetDevicePointer(reinterpret_cast<void **>(&p->err_dev), p->err_host, 0);
+            if (e != hipSuccess)
+                return bail(kvx::hip_fail(e, "hipHostGetDevicePointer(err)", __FILE__, __LINE__));
+
+            if (want_staging) {
+                p->K = K;
+                p->cpb = cpb;
+                p->S = S;
+                const size_t staging_bytes = static_cast<size_t>(K) * cpb * static_cast<size_t>(p->geo.slot_bytes);
+                // Physically contiguous staging: the DMA engines read and write it, and staging placed in
+                // fragmented (recycled) device memory was measured to slow D2H copies by ~5%.  If the
+                // runtime refuses the flag, plain device memory is used and kv_pool_info reports it.
+                e = hipExtMallocWithFlags(reinterpret_cast<void **>(&p->staging), staging_bytes, hipDeviceMallocContiguous);
+                p->staging_contiguous = e == hipSuccess;
+                if (e != hipSuccess) {
+                    (void)hipGetLastError();
+                    e = hipMalloc(reinterpret_cast<void **>(&p->staging), staging_bytes);
+                }
+                if (e != hipSuccess)
+                    return bail(kvx::hip_fail(e, "hipMalloc(staging)", __FILE__, __LINE__));
+                for (int s = 0; s < S; ++s) {
+                    hipStream_t side = nullptr;
+                    // Default priority on purpose: every stream of the library shares one priority.
+                    e = hipStreamCreateWithFlags(&side, hipStreamNonBlocking);
+                    if (e != hipSuccess)
+                        return bail(kvx::hip_fail(e, "hipStreamCreateWithFlags", __FILE__, __LINE__));
+                    p->sides.push_back(side);
+                    hipEvent_t j = nullptr;
+                    if ((st = make_event(&j, false)) != KV_OK)
+                        return bail(st);
+                    p->ev_join.push_back(j);
+                }
+                for (int k = 0; k < K; ++k) {
+                    hipEvent_t a = nullptr, b = nullptr;
+                    if ((st = make_event(&a, false)) != KV_OK)
+                        return bail(st);
+                    p->ev_free.push_back(a);
+                    if ((st = make_event(&b, false)) != KV_OK)
+                        return bail(st);
+                    p->ev_ready.push_back(b);
+                }
+                p->free_recorded.assign(static_cast<size_t>(K), false);
+                if ((st = make_event(&p->ev_entry, false)) != KV_OK)
+                    return bail(st);
+            }
+        } catch (...) {
+            release(p);
+            throw;
         }
-        for (int k = 0; k < K; ++k) {
-            hipEvent_t a = nullptr, b = nullptr;
-            if ((st = make_event(&a, false)) != KV_OK)
-                return bail(st);
-            p->ev_free.push_back(a);
-            if ((st = make_event(&b, false)) != KV_OK)
-                return bail(st);
-            p->ev_ready.push_back(b);
-        }
-        p->free_recorded.assign(static_cast<size_t>(K), false);
-        if ((st = make_event(&p->ev_entry, false)) != KV_OK)
-            return bail(st);
-    }
-    *out = p;
-    return KV_OK;
+        *out = p;
+        return KV_OK;
+    });
 }
 
 kv_status kv_pool_destroy(kv_pool *pool) {
-    if (!pool)
-        return KV_OK;
-    return release(pool);
+    return kvx::guarded([&]() -> kv_status {
+        if (!pool)
+            return KV_OK;
+        return release(pool);
+    });
 }
 
 kv_status kv_pool_get_info(const kv_pool *pool, kv_pool_info *info) {
-    if (!pool || !info)
-        return kvx::fail(KV_EINVAL, "pool and info must not be NULL");
-    std::memset(info, 0, sizeof(*info));
-    info->num_slots = pool->num_slots;
-    info->slot_bytes = pool->geo.slot_bytes;
-    info->pool_bytes = pool->pool_bytes;
-    info->staging_bytes = pool->staging ? static_cast<int64_t>(pool->K) * pool->cpb * pool->geo.slot_bytes : 0;
-    info->alloc_seconds = pool->alloc_seconds;
-    info->device = pool->device;
-    info->mode = pool->mode;
-    info->host_kind = pool->host_kind;
-    info->is_pinned = pool->pinned ? 1 : 0;
-    info->staging_slots = pool->K;
-    info->chunks_per_batch = pool->staging ? pool->cpb : pool->zc_chunks;
-    info->side_streams = pool->S;
-    info->staging_contiguous = pool->staging_contiguous ? 1 : 0;
-    info->host_base = pool->host_base;
-    info->device_base = pool->dev_base;
-    info->num_state_slots = pool->num_state_slots;
-    info->state_slot_bytes = pool->state_slot_bytes;
-    info->state_host_base = pool->num_state_slots > 0 ? pool->host_base + pool->state_offset : nullptr;
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!pool || !info)
+            return kvx::fail(KV_EINVAL, "pool and info must not be NULL");
+        std::memset(info, 0, sizeof(*info));
+        info->num_slots = pool->num_slots;
+        info->slot_bytes = pool->geo.slot_bytes;
+        info->pool_bytes = pool->pool_bytes;
+        info->staging_bytes = pool->staging ? static_cast<int64_t>(pool->K) * pool->cpb * pool->geo.slot_bytes : 0;
+        info->alloc_seconds = pool->alloc_seconds;
+        info->device = pool->device;
+        info->mode = pool->mode;
+        info->host_kind = pool->host_kind;
+        info->is_pinned = pool->pinned ? 1 : 0;
+        info->staging_slots = pool->K;
+        info->chunks_per_batch = pool->staging ? pool->cpb : pool->zc_chunks;
+        info->side_streams = pool->S;
+        info->staging_contiguous = pool->staging_contiguous ? 1 : 0;
+        info->host_base = pool->host_base;
+        info->device_base = pool->dev_base;
+        info->num_state_slots = pool->num_state_slots;
+        info->state_slot_bytes = pool->state_slot_bytes;
+        info->state_host_base = pool->num_state_slots > 0 ? pool->host_base + pool->state_offset : nullptr;
+        return KV_OK;
+    });
 }
 
 void *kv_pool_state_slot(kv_pool *pool, int64_t slot) {
@@ -676,15 +688,17 @@ int64_t kv_pool_slot_bytes(const kv_pool *pool) { return pool ? pool->geo.slot_b
 int64_t kv_pool_num_slots(const kv_pool *pool) { return pool ? pool->num_slots : -1; }
 
 kv_status kv_pool_set_mode(kv_pool *pool, uint32_t mode) {
-    if (!pool)
-        return kvx::fail(KV_EINVAL, "pool must not be NULL");
-    std::lock_guard<std::mutex> lock(pool->mu);
-    if (mode != KV_MODE_ZERO_COPY && mode != KV_MODE_STAGED)
-        return kvx::fail(KV_EINVAL, "unknown mode %u", mode);
-    if (mode == KV_MODE_STAGED && !pool->staging)
-        return kvx::fail(KV_EINVAL, "pool was created without staging; staged mode unavailable");
-    pool->mode = mode;
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!pool)
+            return kvx::fail(KV_EINVAL, "pool must not be NULL");
+        std::lock_guard<std::mutex> lock(pool->mu);
+        if (mode != KV_MODE_ZERO_COPY && mode != KV_MODE_STAGED)
+            return kvx::fail(KV_EINVAL, "unknown mode %u", mode);
+        if (mode == KV_MODE_STAGED && !pool->staging)
+            return kvx::fail(KV_EINVAL, "pool was created without staging; staged mode unavailable");
+        pool->mode = mode;
+        return KV_OK;
+    });
 }
 
 int32_t kv_pool_async_error(kv_pool *pool, int clear) {
@@ -699,51 +713,57 @@ int32_t kv_pool_async_error(kv_pool *pool, int clear) {
 
 kv_status kv_pool_kernel_stats(kv_pool *pool, int which, int reset, int64_t *launches, double *total_ms,
                                double *bytes) {
-    if (!pool || which < 0 || which > 3)
-        return kvx::fail(KV_EINVAL,
-                         "pool must not be NULL and which must be 0 (pack), 1 (unpack), 2 (state pack) or "
-                         "3 (state unpack)");
-    std::lock_guard<std::mutex> lock(pool->mu);
-    auto &pend = pool->pending[which];
-    size_t done = 0;
-    for (; done < pend.size(); ++done) {
-        float ms = 0.0f;
-        hipError_t e = hipEventElapsedTime(&ms, pend[done].start, pend[done].stop);
-        if (e == hipErrorNotReady)
-            break;
-        if (e != hipSuccess)
-            return kvx::hip_fail(e, "hipEventElapsedTime", __FILE__, __LINE__);
-        pool->launches[which] += 1;
-        pool->total_ms[which] += ms;
-        pool->total_bytes[which] += pend[done].bytes;
-        pool->spare_events.push_back(pend[done].start);
-        pool->spare_events.push_back(pend[done].stop);
-    }
-    pend.erase(pend.begin(), pend.begin() + static_cast<std::ptrdiff_t>(done));
-    if (launches)
-        *launches = pool->launches[which];
-    if (total_ms)
-        *total_ms = pool->total_ms[which];
-    if (bytes)
-        *bytes = pool->total_bytes[which];
-    if (reset) {
-        pool->launches[which] = 0;
-        pool->total_ms[which] = 0.0;
-        pool->total_bytes[which] = 0.0;
-    }
-    if (!pend.empty())
-        return kvx::fail(KV_EINVAL, "%zu timed launches have not completed; synchronise first", pend.size());
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!pool || which < 0 || which > 3)
+            return kvx::fail(KV_EINVAL,
+                             "pool must not be NULL and which must be 0 (pack), 1 (unpack), 2 (state pack) or "
+                             "3 (state unpack)");
+        std::lock_guard<std::mutex> lock(pool->mu);
+        auto &pend = pool->pending[which];
+        size_t done = 0;
+        for (; done < pend.size(); ++done) {
+            float ms = 0.0f;
+            hipError_t e = hipEventElapsedTime(&ms, pend[done].start, pend[done].stop);
+            if (e == hipErrorNotReady)
+                break;
+            if (e != hipSuccess)
+                return kvx::hip_fail(e, "hipEventElapsedTime", __FILE__, __LINE__);
+            pool->launches[which] += 1;
+            pool->total_ms[which] += ms;
+            pool->total_bytes[which] += pend[done].bytes;
+            pool->spare_events.push_back(pend[done].start);
+            pool->spare_events.push_back(pend[done].stop);
+        }
+        pend.erase(pend.begin(), pend.begin() + static_cast<std::ptrdiff_t>(done));
+        if (launches)
+            *launches = pool->launches[which];
+        if (total_ms)
+            *total_ms = pool->total_ms[which];
+        if (bytes)
+            *bytes = pool->total_bytes[which];
+        if (reset) {
+            pool->launches[which] = 0;
+            pool->total_ms[which] = 0.0;
+            pool->total_bytes[which] = 0.0;
+        }
+        if (!pend.empty())
+            return kvx::fail(KV_EINVAL, "%zu timed launches have not completed; synchronise first", pend.size());
+        return KV_OK;
+    });
 }
 
 kv_status kv_store(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, kv_pool *pool,
                    const int64_t *chunk_ids, void *stream) {
-    return run(cache, block_table, n_tokens, pool, chunk_ids, stream, kvx::kPack);
+    return kvx::guarded([&]() -> kv_status {
+        return run(cache, block_table, n_tokens, pool, chunk_ids, stream, kvx::kPack);
+    });
 }
 
 kv_status kv_load(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, kv_pool *pool,
                   const int64_t *chunk_ids, void *stream) {
-    return run(cache, block_table, n_tokens, pool, chunk_ids, stream, kvx::kUnpack);
+    return kvx::guarded([&]() -> kv_status {
+        return run(cache, block_table, n_tokens, pool, chunk_ids, stream, kvx::kUnpack);
+    });
 }
 
 }  // extern "C"
@@ -752,12 +772,16 @@ extern "C" {
 
 kv_status kv_store_state(const kv_state *state, const int64_t *pages, int64_t n, kv_pool *pool,
                          const int64_t *slot_ids, void *stream) {
-    return run_state(state, pages, n, pool, slot_ids, stream, kvx::kPack);
+    return kvx::guarded([&]() -> kv_status {
+        return run_state(state, pages, n, pool, slot_ids, stream, kvx::kPack);
+    });
 }
 
 kv_status kv_load_state(const kv_state *state, const int64_t *pages, int64_t n, kv_pool *pool,
                         const int64_t *slot_ids, void *stream) {
-    return run_state(state, pages, n, pool, slot_ids, stream, kvx::kUnpack);
+    return kvx::guarded([&]() -> kv_status {
+        return run_state(state, pages, n, pool, slot_ids, stream, kvx::kUnpack);
+    });
 }
 
 }  // extern "C"

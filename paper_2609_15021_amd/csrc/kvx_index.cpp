@@ -9,6 +9,7 @@
 #include <mutex>
 #include <set>
 #include <unordered_map>
+#include <memory>
 #include <vector>
 
 #include "kvx_internal.h"
@@ -236,257 +237,277 @@ kv_status check_tokens(const kv_index *x, const int32_t *tokens, int64_t n_token
 extern "C" {
 
 kv_status kv_index_create(int32_t chunk_tokens, int64_t num_slots, int64_t num_state_slots, kv_index **out) {
-    if (!out)
-        return kvx::fail(KV_EINVAL, "out must not be NULL");
-    *out = nullptr;
-    if (chunk_tokens < 1 || num_slots < 1 || num_state_slots < 0)
-        return kvx::fail(KV_EINVAL, "need chunk_tokens >= 1, num_slots >= 1, num_state_slots >= 0 (got %d, %lld, %lld)",
-                         chunk_tokens, static_cast<long long>(num_slots), static_cast<long long>(num_state_slots));
-    kv_index *x = new kv_index();
-    x->C = chunk_tokens;
-    x->num_slots = num_slots;
-    x->num_state_slots = num_state_slots;
-    x->e.resize(static_cast<size_t>(num_slots));
-    x->se.resize(static_cast<size_t>(num_state_slots));
-    for (int64_t s = 0; s < num_slots; ++s)
-        x->free_slots.insert(x->free_slots.end(), s);
-    for (int64_t s = 0; s < num_state_slots; ++s)
-        x->free_state.insert(x->free_state.end(), s);
-    x->by_key.reserve(static_cast<size_t>(num_slots) * 2);
-    *out = x;
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!out)
+            return kvx::fail(KV_EINVAL, "out must not be NULL");
+        *out = nullptr;
+        if (chunk_tokens < 1 || num_slots < 1 || num_state_slots < 0)
+            return kvx::fail(KV_EINVAL, "need chunk_tokens >= 1, num_slots >= 1, num_state_slots >= 0 (got %d, %lld, %lld)",
+                             chunk_tokens, static_cast<long long>(num_slots), static_cast<long long>(num_state_slots));
+        std::unique_ptr<kv_index> x(new kv_index());  // freed if a container below throws
+        x->C = chunk_tokens;
+        x->num_slots = num_slots;
+        x->num_state_slots = num_state_slots;
+        x->e.resize(static_cast<size_t>(num_slots));
+        x->se.resize(static_cast<size_t>(num_state_slots));
+        for (int64_t s = 0; s < num_slots; ++s)
+            x->free_slots.insert(x->free_slots.end(), s);
+        for (int64_t s = 0; s < num_state_slots; ++s)
+            x->free_state.insert(x->free_state.end(), s);
+        x->by_key.reserve(static_cast<size_t>(num_slots) * 2);
+        *out = x.release();
+        return KV_OK;
+    });
 }
 
 kv_status kv_index_destroy(kv_index *index) {
-    delete index;
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        delete index;
+        return KV_OK;
+    });
 }
 
 kv_status kv_index_keys(const kv_index *index, uint64_t salt, const int32_t *tokens, int64_t n_tokens,
                         uint64_t *keys) {
-    kv_status st = check_tokens(index, tokens, n_tokens);
-    if (st != KV_OK)
-        return st;
-    const int64_t nfull = n_tokens / index->C;
-    if (nfull > 0 && !keys)
-        return kvx::fail(KV_EINVAL, "keys must not be NULL");
-    KeyChain kc(salt, index->C);
-    for (int64_t i = 0; i < nfull; ++i) {
-        kc.absorb(tokens + i * index->C, index->C);
-        const Key k = kc.key();
-        keys[2 * i] = k.a;
-        keys[2 * i + 1] = k.b;
-    }
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        kv_status st = check_tokens(index, tokens, n_tokens);
+        if (st != KV_OK)
+            return st;
+        const int64_t nfull = n_tokens / index->C;
+        if (nfull > 0 && !keys)
+            return kvx::fail(KV_EINVAL, "keys must not be NULL");
+        KeyChain kc(salt, index->C);
+        for (int64_t i = 0; i < nfull; ++i) {
+            kc.absorb(tokens + i * index->C, index->C);
+            const Key k = kc.key();
+            keys[2 * i] = k.a;
+            keys[2 * i + 1] = k.b;
+        }
+        return KV_OK;
+    });
 }
 
 kv_status kv_index_lookup(kv_index *index, uint64_t salt, const int32_t *tokens, int64_t n_tokens, uint32_t flags,
                           int64_t *slots, kv_lookup *out) {
-    kv_status st = check_tokens(index, tokens, n_tokens);
-    if (st != KV_OK)
-        return st;
-    if (!out)
-        return kvx::fail(KV_EINVAL, "out must not be NULL");
-    if (flags & ~(KV_LOOKUP_REQUIRE_STATE | KV_LOOKUP_PIN))
-        return kvx::fail(KV_EINVAL, "unknown lookup flags 0x%x", flags);
-    kv_index &x = *index;
-    std::lock_guard<std::mutex> lock(x.mu);
-    const int64_t nfull = n_tokens / x.C;
-    if (nfull > 0 && !slots)
-        return kvx::fail(KV_EINVAL, "slots must not be NULL");
-    KeyChain kc(salt, x.C);
-    int64_t kv = 0;
-    for (; kv < nfull; ++kv) {
-        kc.absorb(tokens + kv * x.C, x.C);
-        auto it = x.by_key.find(kc.key());
-        if (it == x.by_key.end() || x.e[it->second].pending)
-            break;
-        slots[kv] = it->second;
-    }
-    auto has_state = [&](int64_t s) { return x.e[s].state >= 0 && !x.e[s].state_pending; };
-    int64_t hit = kv;
-    if (flags & KV_LOOKUP_REQUIRE_STATE)
-        while (hit > 0 && !has_state(slots[hit - 1]))
-            --hit;
-    int64_t state_slot = -1;
-    if (hit > 0 && has_state(slots[hit - 1])) {
-        state_slot = x.e[slots[hit - 1]].state;
-        x.slru.touch(x.se, state_slot);
-    }
-    x.touch_prefix(slots, hit);
-    if (flags & KV_LOOKUP_PIN)
-        for (int64_t j = 0; j < hit; ++j)
-            x.e[slots[j]].pins += 1;
-    out->kv_chunks = kv;
-    out->hit_chunks = hit;
-    out->hit_tokens = hit * x.C;
-    out->state_slot = state_slot;
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        kv_status st = check_tokens(index, tokens, n_tokens);
+        if (st != KV_OK)
+            return st;
+        if (!out)
+            return kvx::fail(KV_EINVAL, "out must not be NULL");
+        if (flags & ~(KV_LOOKUP_REQUIRE_STATE | KV_LOOKUP_PIN))
+            return kvx::fail(KV_EINVAL, "unknown lookup flags 0x%x", flags);
+        kv_index &x = *index;
+        std::lock_guard<std::mutex> lock(x.mu);
+        const int64_t nfull = n_tokens / x.C;
+        if (nfull > 0 && !slots)
+            return kvx::fail(KV_EINVAL, "slots must not be NULL");
+        KeyChain kc(salt, x.C);
+        int64_t kv = 0;
+        for (; kv < nfull; ++kv) {
+            kc.absorb(tokens + kv * x.C, x.C);
+            auto it = x.by_key.find(kc.key());
+            if (it == x.by_key.end() || x.e[it->second].pending)
+                break;
+            slots[kv] = it->second;
+        }
+        auto has_state = [&](int64_t s) { return x.e[s].state >= 0 && !x.e[s].state_pending; };
+        int64_t hit = kv;
+        if (flags & KV_LOOKUP_REQUIRE_STATE)
+            while (hit > 0 && !has_state(slots[hit - 1]))
+                --hit;
+        int64_t state_slot = -1;
+        if (hit > 0 && has_state(slots[hit - 1])) {
+            state_slot = x.e[slots[hit - 1]].state;
+            x.slru.touch(x.se, state_slot);
+        }
+        x.touch_prefix(slots, hit);
+        if (flags & KV_LOOKUP_PIN)
+            for (int64_t j = 0; j < hit; ++j)
+                x.e[slots[j]].pins += 1;
+        out->kv_chunks = kv;
+        out->hit_chunks = hit;
+        out->hit_tokens = hit * x.C;
+        out->state_slot = state_slot;
+        return KV_OK;
+    });
 }
 
 kv_status kv_index_unpin(kv_index *index, const int64_t *slots, int64_t n) {
-    if (!index || n < 0 || (n > 0 && !slots))
-        return kvx::fail(KV_EINVAL, "index and slots must not be NULL, n >= 0");
-    std::lock_guard<std::mutex> lock(index->mu);
-    if (!index->pins_cover(slots, n))
-        return kvx::fail(KV_EINVAL, "a listed slot is not pinned (that often)");
-    for (int64_t i = 0; i < n; ++i)
-        index->release(slots[i]);
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!index || n < 0 || (n > 0 && !slots))
+            return kvx::fail(KV_EINVAL, "index and slots must not be NULL, n >= 0");
+        std::lock_guard<std::mutex> lock(index->mu);
+        if (!index->pins_cover(slots, n))
+            return kvx::fail(KV_EINVAL, "a listed slot is not pinned (that often)");
+        for (int64_t i = 0; i < n; ++i)
+            index->release(slots[i]);
+        return KV_OK;
+    });
 }
 
 kv_status kv_index_reserve(kv_index *index, uint64_t salt, const int32_t *tokens, int64_t n_tokens, int64_t *slots,
                            uint8_t *is_new, int64_t *n_chunks) {
-    kv_status st = check_tokens(index, tokens, n_tokens);
-    if (st != KV_OK)
-        return st;
-    kv_index &x = *index;
-    const int64_t nfull = n_tokens / x.C;
-    if (!n_chunks || (nfull > 0 && (!slots || !is_new)))
-        return kvx::fail(KV_EINVAL, "slots, is_new and n_chunks must not be NULL");
-    std::lock_guard<std::mutex> lock(x.mu);
-    *n_chunks = nfull;
-    KeyChain kc(salt, x.C);
-    for (int64_t i = 0; i < nfull; ++i) {
-        kc.absorb(tokens + i * x.C, x.C);
-        const Key key = kc.key();
-        auto it = x.by_key.find(key);
-        if (it != x.by_key.end()) {
-            x.e[it->second].pins += 1;
-            slots[i] = it->second;
-            is_new[i] = 0;
-            continue;
-        }
-        const int64_t s = x.alloc();
-        if (s < 0) {
-            for (int64_t j = 0; j < i; ++j) {  // undo this call; evictions stand
-                if (is_new[j])
-                    x.drop(slots[j]);
-                else
-                    x.release(slots[j]);
+    return kvx::guarded([&]() -> kv_status {
+        kv_status st = check_tokens(index, tokens, n_tokens);
+        if (st != KV_OK)
+            return st;
+        kv_index &x = *index;
+        const int64_t nfull = n_tokens / x.C;
+        if (!n_chunks || (nfull > 0 && (!slots || !is_new)))
+            return kvx::fail(KV_EINVAL, "slots, is_new and n_chunks must not be NULL");
+        std::lock_guard<std::mutex> lock(x.mu);
+        *n_chunks = nfull;
+        KeyChain kc(salt, x.C);
+        for (int64_t i = 0; i < nfull; ++i) {
+            kc.absorb(tokens + i * x.C, x.C);
+            const Key key = kc.key();
+            auto it = x.by_key.find(key);
+            if (it != x.by_key.end()) {
+                x.e[it->second].pins += 1;
+                slots[i] = it->second;
+                is_new[i] = 0;
+                continue;
             }
-            *n_chunks = 0;
-            return kvx::fail(KV_EBUSY, "no slot can be freed for chunk %lld: all %lld slots are pinned or pending",
-                             static_cast<long long>(i), static_cast<long long>(x.num_slots));
+            const int64_t s = x.alloc();
+            if (s < 0) {
+                for (int64_t j = 0; j < i; ++j) {  // undo this call; evictions stand
+                    if (is_new[j])
+                        x.drop(slots[j]);
+                    else
+                        x.release(slots[j]);
+                }
+                *n_chunks = 0;
+                return kvx::fail(KV_EBUSY, "no slot can be freed for chunk %lld: all %lld slots are pinned or pending",
+                                 static_cast<long long>(i), static_cast<long long>(x.num_slots));
+            }
+            Entry &en = x.e[s];
+            en = Entry{};
+            en.key = key;
+            en.used = true;
+            en.pending = true;
+            en.pins = 1;
+            x.by_key.emplace(key, s);
+            slots[i] = s;
+            is_new[i] = 1;
         }
-        Entry &en = x.e[s];
-        en = Entry{};
-        en.key = key;
-        en.used = true;
-        en.pending = true;
-        en.pins = 1;
-        x.by_key.emplace(key, s);
-        slots[i] = s;
-        is_new[i] = 1;
-    }
-    return KV_OK;
+        return KV_OK;
+    });
 }
 
 kv_status kv_index_commit(kv_index *index, const int64_t *slots, const uint8_t *is_new, int64_t n, int ok) {
-    if (!index || n < 0 || (n > 0 && (!slots || !is_new)))
-        return kvx::fail(KV_EINVAL, "index, slots and is_new must not be NULL, n >= 0");
-    kv_index &x = *index;
-    std::lock_guard<std::mutex> lock(x.mu);
-    std::set<int64_t> seen;
-    for (int64_t i = 0; i < n; ++i) {
-        const int64_t s = slots[i];
-        if (!x.valid_slot(s) || x.e[s].pins == 0 || !seen.insert(s).second)
-            return kvx::fail(KV_EINVAL, "slot %lld is not a distinct pinned entry of this reservation",
-                             static_cast<long long>(s));
-        if (is_new[i] && (!x.e[s].pending || x.e[s].aborted))
-            return kvx::fail(KV_EINVAL, "slot %lld is not a pending entry", static_cast<long long>(s));
-    }
-    for (int64_t i = 0; i < n; ++i) {
-        const int64_t s = slots[i];
-        Entry &en = x.e[s];
-        if (is_new[i]) {
-            if (ok) {
-                en.pending = false;
-                x.lru.push_back(x.e, s);
-            } else {
-                en.aborted = true;
-                x.free_state_of(s);
-                auto it = x.by_key.find(en.key);
-                if (it != x.by_key.end() && it->second == s)
-                    x.by_key.erase(it);
-            }
+    return kvx::guarded([&]() -> kv_status {
+        if (!index || n < 0 || (n > 0 && (!slots || !is_new)))
+            return kvx::fail(KV_EINVAL, "index, slots and is_new must not be NULL, n >= 0");
+        kv_index &x = *index;
+        std::lock_guard<std::mutex> lock(x.mu);
+        std::set<int64_t> seen;
+        for (int64_t i = 0; i < n; ++i) {
+            const int64_t s = slots[i];
+            if (!x.valid_slot(s) || x.e[s].pins == 0 || !seen.insert(s).second)
+                return kvx::fail(KV_EINVAL, "slot %lld is not a distinct pinned entry of this reservation",
+                                 static_cast<long long>(s));
+            if (is_new[i] && (!x.e[s].pending || x.e[s].aborted))
+                return kvx::fail(KV_EINVAL, "slot %lld is not a pending entry", static_cast<long long>(s));
         }
-        x.release(s);
-    }
-    std::vector<int64_t> live;
-    live.reserve(static_cast<size_t>(n));
-    for (int64_t i = 0; i < n; ++i)
-        if (x.e[slots[i]].used && !x.e[slots[i]].pending)
-            live.push_back(slots[i]);
-    x.touch_prefix(live.data(), static_cast<int64_t>(live.size()));
-    return KV_OK;
+        for (int64_t i = 0; i < n; ++i) {
+            const int64_t s = slots[i];
+            Entry &en = x.e[s];
+            if (is_new[i]) {
+                if (ok) {
+                    en.pending = false;
+                    x.lru.push_back(x.e, s);
+                } else {
+                    en.aborted = true;
+                    x.free_state_of(s);
+                    auto it = x.by_key.find(en.key);
+                    if (it != x.by_key.end() && it->second == s)
+                        x.by_key.erase(it);
+                }
+            }
+            x.release(s);
+        }
+        std::vector<int64_t> live;
+        live.reserve(static_cast<size_t>(n));
+        for (int64_t i = 0; i < n; ++i)
+            if (x.e[slots[i]].used && !x.e[slots[i]].pending)
+                live.push_back(slots[i]);
+        x.touch_prefix(live.data(), static_cast<int64_t>(live.size()));
+        return KV_OK;
+    });
 }
 
 kv_status kv_index_reserve_state(kv_index *index, int64_t slot, int64_t *state_slot, int32_t *is_new) {
-    if (!index || !state_slot || !is_new)
-        return kvx::fail(KV_EINVAL, "index, state_slot and is_new must not be NULL");
-    kv_index &x = *index;
-    std::lock_guard<std::mutex> lock(x.mu);
-    if (!x.valid_slot(slot) || x.e[slot].pins == 0 || x.e[slot].aborted)
-        return kvx::fail(KV_EINVAL, "slot %lld is not a pinned entry", static_cast<long long>(slot));
-    Entry &en = x.e[slot];
-    if (en.state >= 0) {
-        *state_slot = en.state;
-        *is_new = 0;
+    return kvx::guarded([&]() -> kv_status {
+        if (!index || !state_slot || !is_new)
+            return kvx::fail(KV_EINVAL, "index, state_slot and is_new must not be NULL");
+        kv_index &x = *index;
+        std::lock_guard<std::mutex> lock(x.mu);
+        if (!x.valid_slot(slot) || x.e[slot].pins == 0 || x.e[slot].aborted)
+            return kvx::fail(KV_EINVAL, "slot %lld is not a pinned entry", static_cast<long long>(slot));
+        Entry &en = x.e[slot];
+        if (en.state >= 0) {
+            *state_slot = en.state;
+            *is_new = 0;
+            return KV_OK;
+        }
+        const int64_t ss = x.alloc_state();
+        if (ss < 0)
+            return kvx::fail(KV_EBUSY, "no snapshot slot can be freed");
+        en.state = ss;
+        en.state_pending = true;
+        x.se[ss].owner = slot;
+        *state_slot = ss;
+        *is_new = 1;
         return KV_OK;
-    }
-    const int64_t ss = x.alloc_state();
-    if (ss < 0)
-        return kvx::fail(KV_EBUSY, "no snapshot slot can be freed");
-    en.state = ss;
-    en.state_pending = true;
-    x.se[ss].owner = slot;
-    *state_slot = ss;
-    *is_new = 1;
-    return KV_OK;
+    });
 }
 
 kv_status kv_index_commit_state(kv_index *index, int64_t slot, int ok) {
-    if (!index)
-        return kvx::fail(KV_EINVAL, "index must not be NULL");
-    kv_index &x = *index;
-    std::lock_guard<std::mutex> lock(x.mu);
-    if (!x.valid_slot(slot) || x.e[slot].state < 0 || !x.e[slot].state_pending)
-        return kvx::fail(KV_EINVAL, "slot %lld has no pending snapshot", static_cast<long long>(slot));
-    Entry &en = x.e[slot];
-    if (ok) {
-        en.state_pending = false;
-        x.slru.push_back(x.se, en.state);
-    } else {
-        x.se[en.state].owner = -1;
-        x.free_state.insert(en.state);
-        en.state = -1;
-        en.state_pending = false;
-    }
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!index)
+            return kvx::fail(KV_EINVAL, "index must not be NULL");
+        kv_index &x = *index;
+        std::lock_guard<std::mutex> lock(x.mu);
+        if (!x.valid_slot(slot) || x.e[slot].state < 0 || !x.e[slot].state_pending)
+            return kvx::fail(KV_EINVAL, "slot %lld has no pending snapshot", static_cast<long long>(slot));
+        Entry &en = x.e[slot];
+        if (ok) {
+            en.state_pending = false;
+            x.slru.push_back(x.se, en.state);
+        } else {
+            x.se[en.state].owner = -1;
+            x.free_state.insert(en.state);
+            en.state = -1;
+            en.state_pending = false;
+        }
+        return KV_OK;
+    });
 }
 
 kv_status kv_index_get_stats(kv_index *index, kv_index_stats *out) {
-    if (!index || !out)
-        return kvx::fail(KV_EINVAL, "index and out must not be NULL");
-    kv_index &x = *index;
-    std::lock_guard<std::mutex> lock(x.mu);
-    std::memset(out, 0, sizeof(*out));
-    for (const Entry &en : x.e) {
-        if (!en.used)
-            continue;
-        if (!en.pending)
-            out->entries += 1;
-        else if (!en.aborted)
-            out->pending += 1;
-    }
-    for (const StateEntry &s : x.se)
-        out->state_entries += s.in_lru ? 1 : 0;
-    out->free_slots = static_cast<int64_t>(x.free_slots.size());
-    out->free_state_slots = static_cast<int64_t>(x.free_state.size());
-    out->evictions = x.evictions;
-    out->state_evictions = x.state_evictions;
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!index || !out)
+            return kvx::fail(KV_EINVAL, "index and out must not be NULL");
+        kv_index &x = *index;
+        std::lock_guard<std::mutex> lock(x.mu);
+        std::memset(out, 0, sizeof(*out));
+        for (const Entry &en : x.e) {
+            if (!en.used)
+                continue;
+            if (!en.pending)
+                out->entries += 1;
+            else if (!en.aborted)
+                out->pending += 1;
+        }
+        for (const StateEntry &s : x.se)
+            out->state_entries += s.in_lru ? 1 : 0;
+        out->free_slots = static_cast<int64_t>(x.free_slots.size());
+        out->free_state_slots = static_cast<int64_t>(x.free_state.size());
+        out->evictions = x.evictions;
+        out->state_evictions = x.state_evictions;
+        return KV_OK;
+    });
 }
 
 }  // extern "C"

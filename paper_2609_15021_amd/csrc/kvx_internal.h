@@ -4,7 +4,9 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <exception>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -89,6 +91,21 @@ int max_chunks_per_launch(const Geometry &g, int nlayers);
 kv_status fail(kv_status code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 kv_status hip_fail(hipError_t err, const char *what, const char *file, int line);
 void set_last_error(const std::string &msg);
+
+// Runs an entry point's body so that no C++ exception crosses the C ABI: a failed host
+// allocation becomes KV_ENOMEM, any other exception KV_EINVAL with its message.
+template <class F>
+kv_status guarded(F &&body) noexcept {
+    try {
+        return body();
+    } catch (const std::bad_alloc &) {
+        return fail(KV_ENOMEM, "host memory allocation failed");
+    } catch (const std::exception &e) {
+        return fail(KV_EINVAL, "internal error: %s", e.what());
+    } catch (...) {
+        return fail(KV_EINVAL, "internal error");
+    }
+}
 
 #define KVX_HIP(expr)                                                         \
     do {                                                                      \

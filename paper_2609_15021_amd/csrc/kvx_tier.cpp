@@ -139,7 +139,8 @@ class Connection {
             }
             if (h.magic != kMagic || h.op < kOpStore || h.op > kOpLoadPrefix || h.num_layers < 1 ||
                 h.num_layers > kMaxLayers || h.n_table < 0 || h.n_chunks < 0 || h.n_ids < 0 ||
-                h.state_layers < 0 || h.state_layers > kMaxLayers)
+                h.state_layers < 0 || h.state_layers > kMaxLayers || h.n_table > kMaxPayload ||
+                h.n_chunks > kMaxPayload || h.n_ids > kMaxPayload)
                 return kvx::fail(KV_EINVAL, "tier: malformed request header");
             const int64_t payload = static_cast<int64_t>(h.num_layers + h.state_layers) * int64_t(sizeof(kv_ipc_buffer)) +
                                     h.n_table * int64_t(sizeof(int32_t)) + h.n_chunks * int64_t(sizeof(int64_t)) +
@@ -195,7 +196,7 @@ class Connection {
             }
             it = opened_.emplace(key, Mapping{base, static_cast<int64_t>(size)}).first;
         }
-        if (buf.offset < 0 || need < 0 || buf.offset + need > it->second.bytes)
+        if (buf.offset < 0 || need < 0 || need > it->second.bytes || buf.offset > it->second.bytes - need)
             return kvx::fail(KV_EINVAL, "tier: %s %d (offset %lld, %lld bytes) exceeds its shared allocation of %lld "
                                         "bytes",
                              what, l, static_cast<long long>(buf.offset), static_cast<long long>(need),
@@ -241,6 +242,8 @@ class Connection {
             return kvx::fail(KV_EINVAL, "tier: num_blocks must be positive");
         layers_.resize(static_cast<size_t>(h.num_layers));
         for (int32_t l = 0; l < h.num_layers; ++l) {
+            if (g.block_stride > INT64_MAX / h.num_blocks)
+                return kvx::fail(KV_EINVAL, "tier: layer extent overflows 64 bits");
             st = open_buffer(bufs_[l], static_cast<int64_t>(h.num_blocks) * g.block_stride, "layer", l,
                              &layers_[static_cast<size_t>(l)]);
             if (st != KV_OK)
@@ -297,7 +300,8 @@ class Connection {
 
     kv_status execute(const RequestHeader &h, int64_t *value, int64_t *value2) {
         const kv_layout &lay = h.layout;
-        if (lay.block_size < 1 || lay.chunk_tokens < 1 || h.n_tokens < 0 || lay.num_layers != h.num_layers)
+        if (lay.block_size < 1 || lay.chunk_tokens < 1 || h.n_tokens < 0 || h.n_tokens > (int64_t{1} << 48) ||
+            lay.num_layers != h.num_layers)
             return kvx::fail(KV_EINVAL, "tier: request layout or length is invalid");
         if (h.n_table != ceil_div(h.n_tokens, lay.block_size))
             return kvx::fail(KV_EINVAL, "tier: block table does not match n_tokens");
@@ -519,129 +523,158 @@ kv_status send_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
 extern "C" {
 
 kv_status kv_ipc_export(const void *dev_ptr, kv_ipc_buffer *out) {
-    if (!dev_ptr || !out)
-        return kvx::fail(KV_EINVAL, "dev_ptr and out must not be NULL");
-    void *base = nullptr;
-    size_t size = 0;
-    KVX_HIP(hipMemGetAddressRange(&base, &size, const_cast<void *>(dev_ptr)));
-    if (static_cast<int64_t>(size) >= KV_IPC_MAX_ALLOCATION_BYTES)
-        return kvx::fail(KV_EUNSUPPORTED,
-                         "allocation of %zu bytes is too large to share between processes (limit %lld); allocate "
-                         "each shared buffer separately",
-                         size, static_cast<long long>(KV_IPC_MAX_ALLOCATION_BYTES));
-    hipIpcMemHandle_t handle;
-    KVX_HIP(hipIpcGetMemHandle(&handle, base));
-    static_assert(sizeof(handle) == sizeof(out->handle), "IPC handle size");
-    std::memcpy(out->handle, &handle, sizeof(handle));
-    out->offset = static_cast<const uint8_t *>(dev_ptr) - static_cast<uint8_t *>(base);
-    out->allocation_bytes = static_cast<int64_t>(size);
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!dev_ptr || !out)
+            return kvx::fail(KV_EINVAL, "dev_ptr and out must not be NULL");
+        void *base = nullptr;
+        size_t size = 0;
+        KVX_HIP(hipMemGetAddressRange(&base, &size, const_cast<void *>(dev_ptr)));
+        if (static_cast<int64_t>(size) >= KV_IPC_MAX_ALLOCATION_BYTES)
+            return kvx::fail(KV_EUNSUPPORTED,
+                             "allocation of %zu bytes is too large to share between processes (limit %lld); allocate "
+                             "each shared buffer separately",
+                             size, static_cast<long long>(KV_IPC_MAX_ALLOCATION_BYTES));
+        hipIpcMemHandle_t handle;
+        KVX_HIP(hipIpcGetMemHandle(&handle, base));
+        static_assert(sizeof(handle) == sizeof(out->handle), "IPC handle size");
+        std::memcpy(out->handle, &handle, sizeof(handle));
+        out->offset = static_cast<const uint8_t *>(dev_ptr) - static_cast<uint8_t *>(base);
+        out->allocation_bytes = static_cast<int64_t>(size);
+        return KV_OK;
+    });
 }
 
 kv_status kv_tier_serve(kv_pool *pool, kv_index *index, int fd) {
-    if (!pool || fd < 0)
-        return kvx::fail(KV_EINVAL, "pool must not be NULL and fd must be a connected socket");
-    Connection c(pool, index, fd);
-    return c.serve();
+    return kvx::guarded([&]() -> kv_status {
+        if (!pool || fd < 0)
+            return kvx::fail(KV_EINVAL, "pool must not be NULL and fd must be a connected socket");
+        Connection c(pool, index, fd);
+        return c.serve();
+    });
 }
 
 kv_status kv_tier_listen(const char *path, int *listen_fd) {
-    if (!path || !listen_fd)
-        return kvx::fail(KV_EINVAL, "path and listen_fd must not be NULL");
-    sockaddr_un addr;
-    std::memset(&addr, 0, sizeof(addr));
-    addr.sun_family = AF_UNIX;
-    if (std::strlen(path) >= sizeof(addr.sun_path))
-        return kvx::fail(KV_EINVAL, "socket path longer than %zu bytes", sizeof(addr.sun_path) - 1);
-    std::strncpy(addr.sun_path, path, sizeof(addr.sun_path) - 1);
-    const int fd = socket(AF_UNIX, SOCK_STREAM, 0);
-    if (fd < 0)
-        return kvx::fail(KV_EINVAL, "socket: %s", std::strerror(errno));
-    if (bind(fd, reinterpret_cast<sockaddr *>(&addr), sizeof(addr)) != 0 || listen(fd, 64) != 0) {
-        const int err = errno;
-        close(fd);
-        return kvx::fail(KV_EINVAL, "cannot listen at %s: %s", path, std::strerror(err));
-    }
-    *listen_fd = fd;
-    return KV_OK;
+    return kvx::guarded([&]() -> kv_status {
+        if (!path || !listen_fd)
+            return kvx::fail(KV_EINVAL, "path and listen_fd must not be NULL");
+        sockaddr_un addr;
+        std::memset(&addr, 0, sizeof(addr));
+        addr.sun_family = AF_UNIX;
+        if (std::strlen(path) >= sizeof(addr.sun_path))
+            return kvx::fail(KV_EINVAL, "socket path longer than %zu bytes", sizeof(addr.sun_path) - 1);
+        std::strncpy(addr.sun_path, path, sizeof(addr.sun_path) - 1);
+        const int fd = socket(AF_UNIX, SOCK_STREAM, 0);
+        if (fd < 0)
+            return kvx::fail(KV_EINVAL, "socket: %s", std::strerror(errno));
+        if (bind(fd, reinterpret_cast<sockaddr *>(&addr), sizeof(addr)) != 0 || listen(fd, 64) != 0) {
+            const int err = errno;
+            close(fd);
+            return kvx::fail(KV_EINVAL, "cannot listen at %s: %s", path, std::strerror(err));
+        }
+        *listen_fd = fd;
+        return KV_OK;
+    });
 }
 
 kv_status kv_tier_run(kv_pool *pool, kv_index *index, int listen_fd, int32_t connections) {
-    if (!pool || listen_fd < 0 || connections < 0)
-        return kvx::fail(KV_EINVAL, "pool must not be NULL, listen_fd a listening socket, connections >= 0");
-    struct Result {
-        kv_status status = KV_OK;
-        std::string message;
-    };
-    std::deque<Result> results;  // push_back keeps references to earlier elements valid
-    std::vector<std::thread> threads;
-    kv_status accept_error = KV_OK;
-    std::string accept_message;
-    for (int32_t k = 0; connections == 0 || k < connections;) {
-        const int fd = accept(listen_fd, nullptr, nullptr);
-        if (fd < 0) {
-            if (errno == EINTR)
-                continue;
-            accept_error = KV_EINVAL;
-            accept_message = std::string("accept: ") + std::strerror(errno);
-            break;
+    return kvx::guarded([&]() -> kv_status {
+        if (!pool || listen_fd < 0 || connections < 0)
+            return kvx::fail(KV_EINVAL, "pool must not be NULL, listen_fd a listening socket, connections >= 0");
+        struct Result {
+            kv_status status = KV_OK;
+            std::string message;
+        };
+        std::deque<Result> results;  // push_back keeps references to earlier elements valid
+        std::vector<std::thread> threads;
+        kv_status accept_error = KV_OK;
+        std::string accept_message;
+        for (int32_t k = 0; connections == 0 || k < connections;) {
+            const int fd = accept(listen_fd, nullptr, nullptr);
+            if (fd < 0) {
+                if (errno == EINTR)
+                    continue;
+                accept_error = KV_EINVAL;
+                accept_message = std::string("accept: ") + std::strerror(errno);
+                break;
+            }
+            ++k;
+            try {
+                results.emplace_back();
+                Result *r = &results.back();
+                threads.emplace_back([pool, index, fd, r] {
+                    r->status = kv_tier_serve(pool, index, fd);
+                    if (r->status != KV_OK) {
+                        try {
+                            r->message = kv_last_error();
+                        } catch (...) {
+                        }
+                    }
+                    close(fd);
+                });
+            } catch (const std::exception &e) {
+                // No thread took this connection: refuse it, stop accepting, and still join the
+                // threads already serving (a joinable thread must never be destroyed).
+                close(fd);
+                accept_error = KV_ENOMEM;
+                accept_message = std::string("cannot serve another connection: ") + e.what();
+                break;
+            }
         }
-        ++k;
-        results.emplace_back();
-        Result *r = &results.back();
-        threads.emplace_back([pool, index, fd, r] {
-            r->status = kv_tier_serve(pool, index, fd);
-            if (r->status != KV_OK)
-                r->message = kv_last_error();
-            close(fd);
-        });
-    }
-    for (std::thread &t : threads)
-        t.join();
-    for (const Result &r : results)
-        if (r.status != KV_OK) {
-            kvx::set_last_error(r.message);
-            return r.status;
-        }
-    if (accept_error != KV_OK)
-        return kvx::fail(accept_error, "%s", accept_message.c_str());
-    return KV_OK;
+        for (std::thread &t : threads)
+            t.join();
+        for (const Result &r : results)
+            if (r.status != KV_OK) {
+                kvx::set_last_error(r.message);
+                return r.status;
+            }
+        if (accept_error != KV_OK)
+            return kvx::fail(accept_error, "%s", accept_message.c_str());
+        return KV_OK;
+    });
 }
 
 kv_status kv_tier_store(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                         const int64_t *chunk_ids, void *stream) {
-    return send_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream, nullptr,
-                        nullptr);
+    return kvx::guarded([&]() -> kv_status {
+        return send_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream, nullptr,
+                            nullptr);
+    });
 }
 
 kv_status kv_tier_load(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                        const int64_t *chunk_ids, void *stream) {
-    return send_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream, nullptr,
-                        nullptr);
+    return kvx::guarded([&]() -> kv_status {
+        return send_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream, nullptr,
+                            nullptr);
+    });
 }
 
 kv_status kv_tier_store_prefix(int fd, const kv_cache *cache, const int32_t *block_table, const kv_state *state,
                                int64_t state_page, uint64_t salt, const int32_t *tokens, int64_t n_tokens,
                                int64_t *stored_chunks, int32_t *stored_state, void *stream) {
-    int64_t v = 0, v2 = 0;
-    const kv_status st = send_request(kOpStorePrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, state,
-                                      state_page, stream, &v, &v2);
-    if (stored_chunks)
-        *stored_chunks = st == KV_OK ? v : 0;
-    if (stored_state)
-        *stored_state = st == KV_OK ? static_cast<int32_t>(v2) : 0;
-    return st;
+    return kvx::guarded([&]() -> kv_status {
+        int64_t v = 0, v2 = 0;
+        const kv_status st = send_request(kOpStorePrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, state,
+                                          state_page, stream, &v, &v2);
+        if (stored_chunks)
+            *stored_chunks = st == KV_OK ? v : 0;
+        if (stored_state)
+            *stored_state = st == KV_OK ? static_cast<int32_t>(v2) : 0;
+        return st;
+    });
 }
 
 kv_status kv_tier_load_prefix(int fd, const kv_cache *cache, const int32_t *block_table, const kv_state *state,
                               int64_t state_page, uint64_t salt, const int32_t *tokens, int64_t n_tokens,
                               int64_t *hit_tokens, void *stream) {
-    int64_t v = 0;
-    const kv_status st = send_request(kOpLoadPrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, state,
-                                      state_page, stream, &v, nullptr);
-    if (hit_tokens)
-        *hit_tokens = st == KV_OK ? v : 0;
-    return st;
+    return kvx::guarded([&]() -> kv_status {
+        int64_t v = 0;
+        const kv_status st = send_request(kOpLoadPrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, state,
+                                          state_page, stream, &v, nullptr);
+        if (hit_tokens)
+            *hit_tokens = st == KV_OK ? v : 0;
+        return st;
+    });
 }
 
 }  // extern "C"

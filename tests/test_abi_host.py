@@ -177,3 +177,17 @@ def test_kv_check_state_agrees_with_oracle_validation():
         assert (got == kvx.KV_OK) == (want == oracle.OK), (G, pb, stride, npages, n, slots, pages, ids, store)
         checked += 1
     assert checked == 400
+
+
+def test_no_exception_crosses_the_c_abi():
+    """A C++ exception inside an entry point comes back as a status code: an index of 2^62 slots
+    makes the library's containers throw (length beyond their maximum), and the call returns an
+    error with a message instead of terminating the process.  Host only (the index makes no GPU
+    call)."""
+    from paper_2609_15021_amd import kvx
+    with pytest.raises(kvx.KvError) as e:
+        kvx.kv_index_create(256, 1 << 62)
+    assert e.value.status in (kvx.KV_EINVAL, kvx.KV_ENOMEM)
+    assert "internal error" in str(e.value) or "allocation failed" in str(e.value)
+    index = kvx.kv_index_create(256, 4)  # the library keeps working
+    kvx.kv_index_destroy(index)

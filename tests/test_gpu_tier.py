@@ -9,6 +9,7 @@ import contextlib
 import gc
 import os
 import socket
+import struct
 import subprocess
 import sys
 import time
@@ -183,17 +184,25 @@ def test_ipc_export_refuses_allocations_of_2_gib():
 
 
 def test_tier_survives_a_malformed_connection(tmp_path):
-    """A connection that sends a garbage frame ends with an error on its own; the tier keeps serving
-    the next replica."""
+    """A connection that sends a garbage frame ends with an error on its own, and so does one whose
+    header announces a block table of 2^62 entries (sizes that would overflow the payload arithmetic);
+    the tier keeps serving the next replica."""
     lay = TINY
     n = 512
     nc, NB = lay.nc(n), 64
     sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
-    p = _start_tier(sock, lay, nc, "staged", 2, dump)
+    p = _start_tier(sock, lay, nc, "staged", 3, dump)
     with _serving(p):
         bad = _connect(sock)
         bad.sendall(b"\x00" * 160)  # a full header's worth of bytes with the wrong magic
         bad.close()
+        # A well-formed load header (magic "KVXT", op 2) with an absurd table length.
+        huge = struct.pack("<II6iiiiiqqqqqQiiqqqq", 0x5458564B, 2, lay.L, lay.H, lay.D, lay.E, lay.BS, lay.C,
+                           NB, 0, lay.L, 0, 0, n, 1 << 62, nc, 0, 0, 0, 0, 0, 0, 0, 0)
+        assert len(huge) == 136
+        bad2 = _connect(sock)
+        bad2.sendall(huge)
+        bad2.close()
         dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
         c = _connect(sock)
         kvx.kv_tier_load(c.fileno(), kvx.Cache(dB, lay.kv, NB), np.arange(lay.nblk(n), dtype=np.int32), n,
@@ -202,8 +211,8 @@ def test_tier_survives_a_malformed_connection(tmp_path):
         out, _ = p.communicate(timeout=90)
     assert p.returncode == 0, out[-2000:]
     results = [ln for ln in out.splitlines() if ln.startswith("TIER")][-1].split(" ", 1)[1].split(";")
-    assert sorted(r == "ok" for r in results) == [False, True], results
-    assert any("malformed" in r for r in results), results
+    assert sorted(r == "ok" for r in results) == [False, False, True], results
+    assert sum("malformed" in r for r in results) == 2, results
 
 
 def _start_native_tier(sock, lay, slots, mode, nconn, dump, index_slots):

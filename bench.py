@@ -1039,24 +1039,34 @@ def main():
         ba, bb = harness.block_table(seed2 + 1, nb2, nblk2), harness.block_table(seed2 + 2, nb2, nblk2)
         ta, tb = torch.from_numpy(ba).to(dev), torch.from_numpy(bb).to(dev)
         ids2 = harness.chunk_ids(nc2, nc2)
-        pool2 = kvx.kv_pool_create(layout, nc2, args.mode, staging_slots=3 if args.mode == "staged" else 0)
-        alloc_s_256k = kvx.kv_pool_get_info(pool2)["alloc_seconds"]
-        torch.cuda.synchronize()  # fills ran on the default stream; s is non-blocking
-        kvx.kv_store(ra.cache, ta, n2, pool2, ids2, s)
-        s.synchronize()
-        times = []
-        for _ in range(3):
-            w0 = time.perf_counter()
-            kvx.kv_load(rb.cache, tb, n2, pool2, ids2, s)
+        try:
+            pool2 = kvx.kv_pool_create(layout, nc2, args.mode, staging_slots=3 if args.mode == "staged" else 0)
+        except kvx.KvError as e:
+            # The 64.06 GiB pool is close to what one process can pin on these machines (about
+            # 65.5 GiB); a machine with less headroom reports it here instead of failing the run.
+            if e.status != kvx.KV_ENOMEM:
+                raise
+            pool2 = None
+            parity_256k = f"not measured: {e}"
+            log(f"[bench] 256k+192 pool could not be pinned: {e}")
+        if pool2 is not None:
+            alloc_s_256k = kvx.kv_pool_get_info(pool2)["alloc_seconds"]
+            torch.cuda.synchronize()  # fills ran on the default stream; s is non-blocking
+            kvx.kv_store(ra.cache, ta, n2, pool2, ids2, s)
             s.synchronize()
-            times.append(time.perf_counter() - w0)
-        restore_256k = statistics.median(times)
-        ok2, msg2 = sampled_round_trip(np, harness, rb, ba, bb, seed2, n2, nb2, [0, nc2 // 2, nc2 - 1], torch)
-        parity_256k = msg2
-        ok = ok and ok2
-        log(f"[bench] 256k+192 restore {restore_256k:.3f} s ({n2 * TOKEN_BYTES / restore_256k / 1e9:.2f} GB/s); "
-            f"parity: {msg2}")
-        kvx.kv_pool_destroy(pool2)
+            times = []
+            for _ in range(3):
+                w0 = time.perf_counter()
+                kvx.kv_load(rb.cache, tb, n2, pool2, ids2, s)
+                s.synchronize()
+                times.append(time.perf_counter() - w0)
+            restore_256k = statistics.median(times)
+            ok2, msg2 = sampled_round_trip(np, harness, rb, ba, bb, seed2, n2, nb2, [0, nc2 // 2, nc2 - 1], torch)
+            parity_256k = msg2
+            ok = ok and ok2
+            log(f"[bench] 256k+192 restore {restore_256k:.3f} s ({n2 * TOKEN_BYTES / restore_256k / 1e9:.2f} GB/s); "
+                f"parity: {msg2}")
+            kvx.kv_pool_destroy(pool2)
         del ra, rb, ta, tb
         torch.cuda.empty_cache()
 

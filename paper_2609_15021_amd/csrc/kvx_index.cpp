@@ -6,10 +6,10 @@
 // restorable only with the recurrent snapshot at its boundary (Sec. 2.2).  The rules where
 // the paper is silent are stated in kvx.h and are the same as the oracle's model.
 #include <cstring>
+#include <memory>
 #include <mutex>
 #include <set>
 #include <unordered_map>
-#include <memory>
 #include <vector>
 
 #include "kvx_internal.h"

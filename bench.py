@@ -92,12 +92,33 @@ def calibrate_copy():
 
 
 class Replica:
-    """One replica's paged cache: [L][NB][2][H][BS][D] bf16 bits in HBM plus its block table."""
+    """One replica's paged cache as a serving engine allocates it: one [NB][2][H][BS][D] tensor per
+    layer (bf16 bits as int16) in HBM.  Values come from the seeded generator with the counter of
+    an element's index in the layer-stacked [L][NB][2][H][BS][D] cache."""
 
     def __init__(self, torch, kvx, layout, num_blocks, dev):
-        self.t = torch.empty((L, num_blocks, 2, H, BS, D), dtype=torch.int16, device=dev)
-        self.cache = kvx.Cache(self.t, layout, num_blocks)
+        self.torch = torch
+        self.layers = [torch.empty((num_blocks, 2, H, BS, D), dtype=torch.int16, device=dev) for _ in range(L)]
+        self.cache = kvx.Cache(self.layers, layout, num_blocks)
         self.num_blocks = num_blocks
+        self.device = dev
+
+    def fill(self, hg, seed, dist):
+        per = self.layers[0].numel()
+        for l, t in enumerate(self.layers):
+            hg.fill_values(t, l * per, seed, dist, E)
+
+    def zero(self):
+        for t in self.layers:
+            t.zero_()
+
+    def blocks(self, idx):
+        """Blocks idx (a device index tensor) of every layer: [L][len(idx)][2][H][BS][D]."""
+        return self.torch.stack([t[idx] for t in self.layers])
+
+    def set_blocks(self, idx, values):
+        for l, t in enumerate(self.layers):
+            t[idx] = values[l]
 
 
 def link_peak(torch, hg, pool_host_ptr, nbytes, dev, reps=10):
@@ -130,8 +151,8 @@ def sampled_round_trip(np, harness, rep_b, bt_a, bt_b, seed, n, num_blocks, chun
         r = min(C, n - i * C)
         nb = -(-r // BS)
         src = harness.gen_blocks(seed, "n01", L, num_blocks, H, BS, D, E, blocks=bt_a[i * bpc:i * bpc + nb])
-        idx = torch.from_numpy(bt_b[i * bpc:i * bpc + nb].astype(np.int64)).to(rep_b.t.device)
-        got = rep_b.t[:, idx].cpu().numpy().view(np.uint16)
+        idx = torch.from_numpy(bt_b[i * bpc:i * bpc + nb].astype(np.int64)).to(rep_b.device)
+        got = rep_b.blocks(idx).cpu().numpy().view(np.uint16)
         if r % BS:  # slots past the prefix end in its last block are not part of the prefix
             got[:, -1, :, :, r % BS:, :] = 0
             src[:, -1, :, :, r % BS:, :] = 0
@@ -458,18 +479,16 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
     finally:
         if tier.poll() is None:
             tier.kill()
-    class PerLayer:  # indexes per-layer buffers as the sampled check indexes a stacked cache
+    class PerLayer:  # the sampled check's view of per-layer buffers
         def __init__(self, layers):
             self.layers, self.device = layers, layers[0].device
 
-        def __getitem__(self, key):
-            return torch.stack([t[key[1]] for t in self.layers])
+        def blocks(self, idx):
+            return torch.stack([t[idx] for t in self.layers])
 
-    stacked = type("Stacked", (), {})()
-    stacked.t = PerLayer(layers_b)
     nc = TIER_N // C
-    ok, msg = sampled_round_trip(np, harness, stacked, bt_a, bt_b, seed, TIER_N, TIER_NB, [0, nc // 2, nc - 1],
-                                 torch)
+    ok, msg = sampled_round_trip(np, harness, PerLayer(layers_b), bt_a, bt_b, seed, TIER_N, TIER_NB,
+                                 [0, nc // 2, nc - 1], torch)
     ok = ok and a_out["stored_chunks"] == nc and all(h == TIER_N for h in hits)
     N = TIER_N * TOKEN_BYTES
     return {"workload": "replica A (a process) stores a 131,072-token prompt of the 27B-class layout by prefix "
@@ -642,7 +661,7 @@ def session_leg(np, torch, harness, hg, kvx, reps, bt_a, layout, mode, dev, turn
             hg.fill_values(fresh, t << 40, seed, "n01", E, sp)
             hg.spin(float(delays[t]), sp)
             with torch.cuda.stream(sp):
-                reps[prod].t[:, torch.from_numpy(extra.astype(np.int64)).to(dev)] = fresh
+                reps[prod].set_blocks(torch.from_numpy(extra.astype(np.int64)).to(dev), fresh)
         else:
             hg.spin(float(delays[t]), sp)
         c0 = n_prev // C
@@ -663,7 +682,7 @@ def session_leg(np, torch, harness, hg, kvx, reps, bt_a, layout, mode, dev, turn
         tp = torch.from_numpy(tables[prod].astype(np.int64)).to(dev)
         tcl = tc.long()
         for k in range(0, nblk, 512):
-            ok = ok and bool(torch.equal(reps[cons].t[:, tcl[k:k + 512]], reps[prod].t[:, tp[k:k + 512]]))
+            ok = ok and bool(torch.equal(reps[cons].blocks(tcl[k:k + 512]), reps[prod].blocks(tp[k:k + 512])))
         out.append({"turn": t, "prefix_tokens": n, "stored_chunks": -(-n // C) - c0,
                     "store_s": round(e0.elapsed_time(e1) / 1e3, 4), "restore_s": round(restore, 4),
                     "restore_GBps": round(n * TOKEN_BYTES / restore / 1e9, 3)})
@@ -886,8 +905,8 @@ def main():
 
     rep_a = Replica(torch, kvx, layout, args.pool_blocks, dev)
     rep_b = Replica(torch, kvx, layout, args.pool_blocks, dev)
-    hg.fill_values(rep_a.t, 0, seed, "n01", E)
-    rep_b.t.zero_()
+    rep_a.fill(hg, seed, "n01")
+    rep_b.zero()
     bt_a = harness.block_table(seed + 1, args.pool_blocks, nblk)
     bt_b = harness.block_table(seed + 2, args.pool_blocks, nblk)
     t_a, t_b = torch.from_numpy(bt_a).to(dev), torch.from_numpy(bt_b).to(dev)
@@ -1034,8 +1053,8 @@ def main():
         nc2, nblk2 = -(-n2 // C), -(-n2 // BS)
         seed2 = harness.sub_seed("bench", n2)
         ra, rb = Replica(torch, kvx, layout, nb2, dev), Replica(torch, kvx, layout, nb2, dev)
-        hg.fill_values(ra.t, 0, seed2, "n01", E)
-        rb.t.zero_()
+        ra.fill(hg, seed2, "n01")
+        rb.zero()
         ba, bb = harness.block_table(seed2 + 1, nb2, nblk2), harness.block_table(seed2 + 2, nb2, nblk2)
         ta, tb = torch.from_numpy(ba).to(dev), torch.from_numpy(bb).to(dev)
         ids2 = harness.chunk_ids(nc2, nc2)
@@ -1099,9 +1118,10 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u8", "data": "synthetic",
         "config": {"workload": "27B-class GQA KV cache (64 layers, 8 KV heads, head_dim 128, bf16 values moved as "
-                               "opaque bytes, 16-token blocks): store a 131,072-token prefix from 8,192 random blocks "
-                               "of a 10,240-block allocation into 512 pinned 256-token chunks, then load it into a "
-                               "fresh random 8,192-block set of a second allocation",
+                               "opaque bytes, 16-token blocks, one tensor per layer as a serving engine allocates it): "
+                               "store a 131,072-token prefix from 8,192 random blocks of a 10,240-block cache into 512 "
+                               "pinned 256-token chunks, then load it into a fresh random 8,192-block set of a second "
+                               "replica's cache",
                    "prefix_tokens": n, "bytes_per_direction": N, "mode": args.mode, "parallelism": "single GPU"},
         "store_GBps": round(store_gbps, 3), "load_GBps": round(load_gbps, 3),
         "restore_s_128k": round(restore_128k, 4),

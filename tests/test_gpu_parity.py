@@ -11,7 +11,7 @@ import torch
 import harness
 from harness import gpu as hg
 from paper_2609_15021_amd import kvx
-from tests.gpu_support import (DEV, TINY, Layout, bt_tensor, device_cache, first_mismatch, host_cache,
+from tests.gpu_support import (DEV, TINY, TORCH_INT, Layout, bt_tensor, device_cache, first_mismatch, host_cache,
                                oracle_pool, oracle_unpack_into, to_device, to_host)
 
 pytestmark = pytest.mark.gpu
@@ -207,6 +207,43 @@ def test_out_of_range_block_is_flagged_and_skipped(mode):
     want = oracle_pool(lay, spare, bt0, n, [0, 1], 2, POOL_SENT)
     assert np.array_equal(view, want), first_mismatch(view, want)
     assert kvx.kv_pool_async_error(pool, clear=True) == kvx.KV_ASYNC_BAD_BLOCK
+    assert kvx.kv_pool_async_error(pool) == 0
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+@pytest.mark.parametrize("dims", [(2, 2, 64, 2, 16, 256), (70, 1, 8, 2, 16, 256)], ids=["tiny", "70-layers"])
+def test_per_layer_allocations(mode, dims):
+    """Caches held as one device allocation per layer (as a serving engine allocates them, and as
+    the tier's replicas and the benchmark use them): store from separate per-layer tensors, load
+    into separate per-layer tensors of another replica; pool and caches equal the oracle's bytes.
+    70 layers also splits the launch's layer pointers across two launches."""
+    lay = Layout(*dims)
+    NB, n = 96, 5 * lay.C + 33
+    seed = harness.sub_seed("parity", "per-layer", mode, lay.L)
+    A = host_cache(lay, NB, seed, "raw")
+    nblk, nc = lay.nblk(n), lay.nc(n)
+    btA, btB = harness.block_table(seed + 1, NB, nblk), harness.block_table(seed + 2, NB, nblk)
+    cid = harness.chunk_ids(nc, nc + 1, seed + 3)
+    pool = kvx.kv_pool_create(lay.kv, nc + 1, mode, staging_slots=2, chunks_per_batch=2)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    la = [to_device(np.ascontiguousarray(A[l])) for l in range(lay.L)]
+    lb = [torch.empty((NB, 2, lay.H, lay.BS, lay.D), dtype=TORCH_INT[lay.E], device=DEV) for _ in range(lay.L)]
+    for t in lb:
+        t.view(torch.uint8).fill_(CACHE_SENT)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    kvx.kv_store(kvx.Cache(la, lay.kv, NB), bt_tensor(btA), n, pool, cid, s)
+    kvx.kv_load(kvx.Cache(lb, lay.kv, NB), bt_tensor(btB), n, pool, cid, s)
+    s.synchronize()
+    want_pool = oracle_pool(lay, A, btA, n, cid, nc + 1, POOL_SENT)
+    assert np.array_equal(view, want_pool), "pool: " + first_mismatch(view, want_pool)
+    B0 = np.full(A.shape, 0, dtype=A.dtype)
+    B0.view(np.uint8)[:] = CACHE_SENT
+    want_B = oracle_unpack_into(lay, B0, btB, n, want_pool, cid)
+    got_B = torch.stack(lb).cpu().numpy().view(A.dtype).reshape(A.shape)
+    assert np.array_equal(got_B, want_B), "cache B: " + first_mismatch(got_B, want_B)
     assert kvx.kv_pool_async_error(pool) == 0
     kvx.kv_pool_destroy(pool)
 

@@ -71,8 +71,23 @@ def build_harness(verbose: bool = False) -> str:
     return LIB_HARNESS
 
 
+NATIVE_SRC = os.path.join(ROOT, "tests", "native", "kvx_native_caller.c")
+NATIVE_BIN = os.path.join(ROOT, "tests", "native", "kvx_native_caller")
+
+
+def build_native_caller(verbose: bool = False) -> str:
+    """The tests' native C caller of the C ABI (plain C against kvx.h and the HIP C API)."""
+    tmp = NATIVE_BIN + ".tmp"
+    _run(["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE,
+          "-I", "/opt/rocm/include", NATIVE_SRC, "-o", tmp, "-L", PKG, "-lkvx",
+          "-Wl,-rpath,$ORIGIN/../../paper_2609_15021_amd", "-L", "/opt/rocm/lib", "-Wl,-rpath,/opt/rocm/lib",
+          "-lamdhip64"], verbose)
+    os.replace(tmp, NATIVE_BIN)
+    return NATIVE_BIN
+
+
 def build_all(verbose: bool = False):
-    return build_kvx(verbose), build_harness(verbose)
+    return build_kvx(verbose), build_harness(verbose), build_native_caller(verbose)
 
 
 if __name__ == "__main__":

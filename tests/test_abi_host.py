@@ -191,3 +191,15 @@ def test_no_exception_crosses_the_c_abi():
     assert "internal error" in str(e.value) or "allocation failed" in str(e.value)
     index = kvx.kv_index_create(256, 4)  # the library keeps working
     kvx.kv_index_destroy(index)
+
+
+def test_native_caller_links_against_the_library(tmp_path):
+    """The tests' native C caller is built against libkvx.so and starts without the Python binding;
+    with no input files it stops before any HIP call and says so (no GPU is touched)."""
+    from paper_2609_15021_amd import build
+    assert os.path.exists(build.NATIVE_BIN), "native caller not built; run __graft_entry__.build()"
+    ldd = subprocess.run(["ldd", build.NATIVE_BIN], capture_output=True, text=True, check=True).stdout
+    assert "libkvx.so" in ldd and "not found" not in ldd, ldd
+    r = subprocess.run([build.NATIVE_BIN, "staged", "2", "2", "64", "2", "16", "256", "8", "16", "1", str(tmp_path)],
+                       capture_output=True, text=True, timeout=60)
+    assert r.returncode == 1 and "cannot read the inputs" in r.stderr, r.stderr

@@ -72,6 +72,7 @@ def parse():
     ap.add_argument("--paper-hybrid-server", metavar="SOCKET", help=argparse.SUPPRESS)
     ap.add_argument("--paper-hybrid-store", metavar="SOCKET", help=argparse.SUPPRESS)
     ap.add_argument("--tier-server", metavar="SOCKET", help=argparse.SUPPRESS)
+    ap.add_argument("--tier-load-mode", choices=["staged", "zero_copy"], help=argparse.SUPPRESS)
     ap.add_argument("--tier-store", metavar="SOCKET", help=argparse.SUPPRESS)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (PMC counter scale reference)")
@@ -398,9 +399,12 @@ def layer_caches(torch, hg, kvx, nb, dev, seed=None):
     return layers, kvx.Cache(layers, kvx.make_layout(L, H, D, E, BS, C), nb)
 
 
-def tier_server(torch, kvx, sock, mode):
-    """The tier process: the pool, a pool index over its slots, the library's own listener."""
+def tier_server(torch, kvx, sock, mode, load_mode=None):
+    """The tier process: the pool, a pool index over its slots, the library's own listener.  With
+    load_mode, loads use that mode and stores `mode`."""
     pool = kvx.kv_pool_create(kvx.make_layout(L, H, D, E, BS, C), -(-TIER_N // C), mode, profile=True)
+    if load_mode:
+        kvx.kv_pool_set_modes(pool, mode, load_mode)
     index = kvx.kv_index_create(C, -(-TIER_N // C))
     fd = kvx.kv_tier_listen(sock)
     print("READY", flush=True)
@@ -436,7 +440,7 @@ def tier_store(np, torch, harness, hg, kvx, sock, dev):
     print(json.dumps({"store_s": dt, "stored_chunks": stored}), flush=True)
 
 
-def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
+def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
     """Replica A (a process) stores a 128k-token prompt by prefix through a tier process that owns
     the pool and its index; replica B (this process) asks for the same prompt and restores its
     external hit: host wall clock of each request, keying and handshake included."""
@@ -446,7 +450,8 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
     tmp = tempfile.mkdtemp(prefix="kvx_tier_")
     sock = os.path.join(tmp, "tier.sock")
     me = os.path.abspath(__file__)
-    tier = subprocess.Popen([sys.executable, "-u", me, "--tier-server", sock, "--mode", mode],
+    tier = subprocess.Popen([sys.executable, "-u", me, "--tier-server", sock, "--mode", mode,
+                             *(["--tier-load-mode", load_mode] if load_mode else [])],
                             stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
     try:
         line = tier.stdout.readline()
@@ -495,7 +500,7 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
                         "through a tier process that owns the pinned pool and its index; replica B (another "
                         "process) asks for the same prompt and restores its external hit; caches shared by HIP IPC, "
                         "one allocation per layer; host-side completion at both ends",
-            "mode": mode, "stored_chunks": a_out["stored_chunks"], "external_hit_tokens": hits[0],
+            "mode": mode if not load_mode else f"{mode} stores, {load_mode} loads", "stored_chunks": a_out["stored_chunks"], "external_hit_tokens": hits[0],
             "store_s": round(store_s, 4), "store_GBps": round(N / store_s / 1e9, 3),
             "restore_s_first": round(restore[0], 4), "restore_s": round(statistics.median(restore[1:] or restore), 4),
             "restore_GBps": round(N / statistics.median(restore[1:] or restore) / 1e9, 3),
@@ -839,7 +844,7 @@ def main():
         print(json.dumps(res), flush=True)
         sys.exit(0 if res_ok else 1)
     if args.tier_server:
-        tier_server(torch, kvx, args.tier_server, args.mode)
+        tier_server(torch, kvx, args.tier_server, args.mode, args.tier_load_mode)
         return
     if args.tier_store:
         tier_store(np, torch, harness, hg, kvx, args.tier_store, dev)
@@ -847,10 +852,12 @@ def main():
     if args.tier_only:
         # Both modes: across processes zero-copy was measured faster than staged (the staged
         # host-to-device copies slow down while kernels write IPC-imported caches).
+        # Also staged stores with zero-copy loads: the faster mode of each direction (one pool).
         res, res_ok = {}, True
-        for mode in ("zero_copy", "staged"):
-            r, ok_m = tier_leg(np, torch, harness, hg, kvx, mode, dev)
-            res[mode] = r
+        for key, mode, load_mode in (("zero_copy", "zero_copy", None), ("staged", "staged", None),
+                                     ("staged_store_zero_copy_load", "staged", "zero_copy")):
+            r, ok_m = tier_leg(np, torch, harness, hg, kvx, mode, dev, load_mode=load_mode)
+            res[key] = r
             res_ok = res_ok and ok_m
         print(json.dumps(res), flush=True)
         sys.exit(0 if res_ok else 1)

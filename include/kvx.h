@@ -147,7 +147,7 @@ typedef struct kv_pool_info {
     int64_t staging_bytes;     /* device staging (0 without staging) */
     double alloc_seconds;      /* wall time of the pinned allocation (cf. Sec. 3.3) */
     int32_t device;
-    uint32_t mode;
+    uint32_t mode;             /* mode of stores (and of loads unless kv_pool_set_modes split them) */
     uint32_t host_kind;
     int32_t is_pinned;         /* 1: the runtime reports the pool as pinned host memory */
     int32_t staging_slots;
@@ -160,6 +160,8 @@ typedef struct kv_pool_info {
     int64_t state_slot_bytes;
     void *state_host_base;     /* host address of state slot 0 (NULL without a state area); the
                                   state area follows the chunk slots in the same pinned region */
+    uint32_t load_mode;        /* mode of loads; `mode` above is the mode of stores */
+    uint32_t pad;
 } kv_pool_info;
 
 /* A replica's recurrent-state page buffers (hybrid models).  The caller owns all memory. */
@@ -202,8 +204,14 @@ KV_API void *kv_pool_slot(kv_pool *pool, int64_t slot);
 KV_API int64_t kv_pool_slot_bytes(const kv_pool *pool);  /* -1 on NULL */
 KV_API int64_t kv_pool_num_slots(const kv_pool *pool);   /* -1 on NULL */
 
-/* Switch mode between calls.  KV_EINVAL for an unknown mode or staged mode without staging. */
+/* Switch mode between calls, for stores and loads alike.  KV_EINVAL for an unknown mode or staged
+ * mode without staging. */
 KV_API kv_status kv_pool_set_mode(kv_pool *pool, uint32_t mode);
+
+/* Switch mode between calls, separately for stores and loads (e.g. a tier that stores staged and
+ * restores zero-copy, the faster mode of each direction across processes).  The pool reports both
+ * in kv_pool_info.  Same errors as kv_pool_set_mode. */
+KV_API kv_status kv_pool_set_modes(kv_pool *pool, uint32_t store_mode, uint32_t load_mode);
 
 /*
  * Device-side faults seen since the last clear (bitmask of KV_ASYNC_*; 0 if

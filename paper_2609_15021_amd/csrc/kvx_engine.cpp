@@ -250,7 +250,7 @@ kv_status transfer(kv_pool *p, const kv_cache *cache, const int32_t *block_table
     const Geometry &g = p->geo;
     const int64_t nc = (n_tokens + g.C - 1) / g.C;
 
-    if (p->mode == KV_MODE_ZERO_COPY) {
+    if (p->mode_of[dir] == KV_MODE_ZERO_COPY) {
         std::vector<int32_t> slots(static_cast<size_t>(nc));
         for (int64_t i = 0; i < nc; ++i)
             slots[static_cast<size_t>(i)] = static_cast<int32_t>(chunk_ids[i]);
@@ -356,7 +356,7 @@ kv_status enqueue_state(kv_pool *p, const kv_state *st, const StatePlan &plan, c
 kv_status transfer_state(kv_pool *p, const kv_state *st, const int64_t *pages, int64_t n, const int64_t *slot_ids,
                          hipStream_t stream, Direction dir) {
     const int64_t S = p->state_slot_bytes;
-    if (p->mode == KV_MODE_ZERO_COPY) {
+    if (p->mode_of[dir] == KV_MODE_ZERO_COPY) {
         const StatePlan plan(st, n, kvx::kStatePiece);
         auto off = [&](int64_t k) { return slot_ids[k] * S; };
         return enqueue_state(p, st, plan, pages, 0, plan.pieces, p->dev_base + p->state_offset, off, true, stream,
@@ -529,7 +529,7 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
             p->num_state_slots > 0 ? p->state_offset + p->num_state_slots * p->state_slot_bytes : p->pool_bytes;
         // From here on the pool owns runtime resources: release them if a host container throws.
         try {
-            p->mode = opts->mode;
+            p->mode_of[kvx::kPack] = p->mode_of[kvx::kUnpack] = opts->mode;
             p->host_kind = opts->host_kind;
             p->profile = opts->profile != 0;
             p->zc_chunks = zc_chunks;
@@ -655,7 +655,8 @@ kv_status kv_pool_get_info(const kv_pool *pool, kv_pool_info *info) {
         info->staging_bytes = pool->staging ? static_cast<int64_t>(pool->K) * pool->cpb * pool->geo.slot_bytes : 0;
         info->alloc_seconds = pool->alloc_seconds;
         info->device = pool->device;
-        info->mode = pool->mode;
+        info->mode = pool->mode_of[kvx::kPack];
+        info->load_mode = pool->mode_of[kvx::kUnpack];
         info->host_kind = pool->host_kind;
         info->is_pinned = pool->pinned ? 1 : 0;
         info->staging_slots = pool->K;
@@ -687,19 +688,24 @@ int64_t kv_pool_slot_bytes(const kv_pool *pool) { return pool ? pool->geo.slot_b
 
 int64_t kv_pool_num_slots(const kv_pool *pool) { return pool ? pool->num_slots : -1; }
 
-kv_status kv_pool_set_mode(kv_pool *pool, uint32_t mode) {
+kv_status kv_pool_set_modes(kv_pool *pool, uint32_t store_mode, uint32_t load_mode) {
     return kvx::guarded([&]() -> kv_status {
         if (!pool)
             return kvx::fail(KV_EINVAL, "pool must not be NULL");
         std::lock_guard<std::mutex> lock(pool->mu);
-        if (mode != KV_MODE_ZERO_COPY && mode != KV_MODE_STAGED)
-            return kvx::fail(KV_EINVAL, "unknown mode %u", mode);
-        if (mode == KV_MODE_STAGED && !pool->staging)
-            return kvx::fail(KV_EINVAL, "pool was created without staging; staged mode unavailable");
-        pool->mode = mode;
+        for (uint32_t mode : {store_mode, load_mode}) {
+            if (mode != KV_MODE_ZERO_COPY && mode != KV_MODE_STAGED)
+                return kvx::fail(KV_EINVAL, "unknown mode %u", mode);
+            if (mode == KV_MODE_STAGED && !pool->staging)
+                return kvx::fail(KV_EINVAL, "pool was created without staging; staged mode unavailable");
+        }
+        pool->mode_of[kvx::kPack] = store_mode;
+        pool->mode_of[kvx::kUnpack] = load_mode;
         return KV_OK;
     });
 }
+
+kv_status kv_pool_set_mode(kv_pool *pool, uint32_t mode) { return kv_pool_set_modes(pool, mode, mode); }
 
 int32_t kv_pool_async_error(kv_pool *pool, int clear) {
     if (!pool)

@@ -137,7 +137,8 @@ struct kv_pool {
     // state_offset bytes into the pinned region (after the chunk slots).
     int64_t num_state_slots = 0, state_slot_bytes = 0, state_offset = 0;
     int device = 0;
-    uint32_t mode = 0, host_kind = 0;
+    uint32_t mode_of[2] = {0, 0};     // transfer mode per direction: [kPack] stores, [kUnpack] loads
+    uint32_t host_kind = 0;
     uint8_t *host_base = nullptr;   // host address of slot 0
     uint8_t *dev_base = nullptr;    // device address of slot 0
     int32_t *err_host = nullptr;    // async error word (pinned, mapped)

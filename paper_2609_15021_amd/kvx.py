@@ -68,7 +68,8 @@ class KvPoolInfo(ctypes.Structure):
                 ("chunks_per_batch", ctypes.c_int32), ("side_streams", ctypes.c_int32),
                 ("staging_contiguous", ctypes.c_int32), ("host_base", ctypes.c_void_p),
                 ("device_base", ctypes.c_void_p), ("num_state_slots", ctypes.c_int64),
-                ("state_slot_bytes", ctypes.c_int64), ("state_host_base", ctypes.c_void_p)]
+                ("state_slot_bytes", ctypes.c_int64), ("state_host_base", ctypes.c_void_p),
+                ("load_mode", ctypes.c_uint32), ("pad", ctypes.c_uint32)]
 
 
 class KvState(ctypes.Structure):
@@ -110,6 +111,7 @@ def _open():
         "kv_pool_slot_bytes": ([P], i64),
         "kv_pool_num_slots": ([P], i64),
         "kv_pool_set_mode": ([P, u32], i32),
+        "kv_pool_set_modes": ([P, u32, u32], i32),
         "kv_pool_async_error": ([P, ctypes.c_int], i32),
         "kv_pool_kernel_stats": ([P, ctypes.c_int, ctypes.c_int, ctypes.POINTER(i64),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)], i32),
@@ -154,7 +156,7 @@ def _open():
 _lib = _open()
 
 EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slot", "kv_pool_slot_bytes",
-           "kv_pool_num_slots", "kv_pool_set_mode", "kv_pool_async_error", "kv_pool_kernel_stats", "kv_check",
+           "kv_pool_num_slots", "kv_pool_set_mode", "kv_pool_set_modes", "kv_pool_async_error", "kv_pool_kernel_stats", "kv_check",
            "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version", "kv_pool_state_slot",
            "kv_check_state", "kv_store_state", "kv_load_state", "kv_index_create", "kv_index_destroy",
            "kv_index_keys", "kv_index_lookup", "kv_index_unpin", "kv_index_reserve", "kv_index_commit",
@@ -277,6 +279,12 @@ def kv_pool_num_slots(pool: Pool) -> int:
 
 def kv_pool_set_mode(pool: Pool, mode) -> None:
     _raise(_lib.kv_pool_set_mode(pool.handle, MODES[mode] if isinstance(mode, str) else int(mode)))
+
+
+def kv_pool_set_modes(pool: Pool, store_mode, load_mode) -> None:
+    def code(m):
+        return MODES[m] if isinstance(m, str) else int(m)
+    _raise(_lib.kv_pool_set_modes(pool.handle, code(store_mode), code(load_mode)))
 
 
 def kv_pool_async_error(pool: Pool, clear: bool = False) -> int:

@@ -248,6 +248,59 @@ def test_per_layer_allocations(mode, dims):
     kvx.kv_pool_destroy(pool)
 
 
+@pytest.mark.parametrize("store_mode,load_mode", [("staged", "zero_copy"), ("zero_copy", "staged")])
+def test_separate_store_and_load_modes(store_mode, load_mode):
+    """kv_pool_set_modes gives stores and loads their own mode.  On one stream with no host sync in
+    between: store (one mode), load (the other), then a second store of other chunks and a load of
+    them; pools and caches equal the oracle's bytes, and the pool reports both modes."""
+    lay = TINY
+    NB, n = 512, 4096 + 192
+    seed = harness.sub_seed("parity", "modes", store_mode)
+    A = host_cache(lay, NB, seed, "raw")
+    nblk, nc = lay.nblk(n), lay.nc(n)
+    btA, btB = harness.block_table(seed + 1, NB, nblk), harness.block_table(seed + 2, NB, nblk)
+    num_slots = 2 * nc
+    ids = harness.chunk_ids(2 * nc, num_slots, seed + 3)
+    pool = kvx.kv_pool_create(lay.kv, num_slots, "staged", staging_slots=2, chunks_per_batch=2)
+    kvx.kv_pool_set_modes(pool, store_mode, load_mode)
+    info = kvx.kv_pool_get_info(pool)
+    assert (info["mode"], info["load_mode"]) == (kvx.MODES[store_mode], kvx.MODES[load_mode])
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    dA = to_device(A)
+    dB1, dB2 = device_cache(lay, NB, fill=CACHE_SENT), device_cache(lay, NB, fill=CACHE_SENT)
+    cA, cB1, cB2 = (kvx.Cache(d, lay.kv, NB) for d in (dA, dB1, dB2))
+    tA, tB = bt_tensor(btA), bt_tensor(btB)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    kvx.kv_store(cA, tA, n, pool, ids[:nc], s)
+    kvx.kv_load(cB1, tB, n, pool, ids[:nc], s)
+    kvx.kv_store(cA, tB, n, pool, ids[nc:], s)  # other blocks of A into the other slots
+    kvx.kv_load(cB2, tA, n, pool, ids[nc:], s)
+    s.synchronize()
+    want = oracle_pool(lay, A, btA, n, ids[:nc], num_slots, POOL_SENT)
+    other = oracle_pool(lay, A, btB, n, ids[nc:], num_slots, POOL_SENT)
+    for i in ids[nc:]:
+        want[i * lay.slot_bytes:(i + 1) * lay.slot_bytes] = other[i * lay.slot_bytes:(i + 1) * lay.slot_bytes]
+    assert np.array_equal(view, want), "pool: " + first_mismatch(view, want)
+    B0 = np.full(A.shape, 0, dtype=A.dtype)
+    B0.view(np.uint8)[:] = CACHE_SENT
+    for got_t, bt, cid in ((dB1, btB, ids[:nc]), (dB2, btA, ids[nc:])):
+        want_B = oracle_unpack_into(lay, B0, bt, n, want, cid)
+        got = to_host(got_t, A)
+        assert np.array_equal(got, want_B), "cache: " + first_mismatch(got, want_B)
+    kvx.kv_pool_set_mode(pool, "zero_copy")
+    info = kvx.kv_pool_get_info(pool)
+    assert info["mode"] == info["load_mode"] == kvx.KV_MODE_ZERO_COPY
+    kvx.kv_pool_destroy(pool)
+    zc = kvx.kv_pool_create(lay.kv, 2, "zero_copy")  # no staging: staged is refused in either direction
+    for modes in (("staged", "zero_copy"), ("zero_copy", "staged")):
+        with pytest.raises(kvx.KvError) as e:
+            kvx.kv_pool_set_modes(zc, *modes)
+        assert e.value.status == kvx.KV_EINVAL
+    kvx.kv_pool_destroy(zc)
+
+
 @pytest.mark.parametrize("mode", ["zero_copy", "staged"])
 def test_concurrent_store_and_load_on_two_streams(mode):
     """Two replicas use one pool at once: one stores prefix Q into slots Y on stream s1 while

@@ -535,10 +535,12 @@ def paper_hybrid_cache(torch, hg, kvx, dev, seed=None, state_seed=None):
     return layers, pages, kvx.Cache(layers, lay, PH["NB"]), kvx.State(pages, GDN_PAGE, 2)
 
 
-def paper_hybrid_server(kvx, sock, mode):
+def paper_hybrid_server(kvx, sock, mode, load_mode=None):
     lay = kvx.make_layout(PH["L"], PH["H"], PH["D"], PH["E"], PH["BS"], PH["C"])
     slots = -(-PH["N"] // PH["C"])
     pool = kvx.kv_pool_create(lay, slots, mode, num_state_slots=2, state_slot_bytes=GDN_LAYERS * GDN_PAGE)
+    if load_mode:
+        kvx.kv_pool_set_modes(pool, mode, load_mode)
     index = kvx.kv_index_create(PH["C"], slots, 2)
     fd = kvx.kv_tier_listen(sock)
     print("READY", flush=True)
@@ -569,7 +571,7 @@ def paper_hybrid_store(torch, harness, hg, kvx, sock, dev):
     print(json.dumps({"store_s": dt, "stored_chunks": stored, "stored_state": stored_state}), flush=True)
 
 
-def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
+def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
     """Replica A stores the paper's 128,000-token hybrid prompt through the tier (chunks and the
     boundary snapshot); replica B asks for the same prompt under aligned recovery."""
     import socket
@@ -577,7 +579,8 @@ def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
     import tempfile
     sock = os.path.join(tempfile.mkdtemp(prefix="kvx_ph_"), "tier.sock")
     me = os.path.abspath(__file__)
-    tier = subprocess.Popen([sys.executable, "-u", me, "--paper-hybrid-server", sock, "--mode", mode],
+    tier = subprocess.Popen([sys.executable, "-u", me, "--paper-hybrid-server", sock, "--mode", mode,
+                             *(["--tier-load-mode", load_mode] if load_mode else [])],
                             stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
     try:
         if not tier.stdout.readline().startswith("READY"):
@@ -630,7 +633,7 @@ def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
                         "(4 KV heads, head_dim 256, 32-token HND pages), 1,568-token chunks, 48 recurrent layers with "
                         "3 MiB + 60 KiB snapshot pages; a 128,000-token prompt stored by replica A with its boundary "
                         "snapshot and restored by replica B under aligned recovery",
-            "mode": mode, "external_hit_tokens": hits[0], "stored_chunks": a_out["stored_chunks"],
+            "mode": mode if not load_mode else f"{mode} stores, {load_mode} loads", "external_hit_tokens": hits[0], "stored_chunks": a_out["stored_chunks"],
             "bytes_restored": attn + snap, "store_s": round(a_out["store_s"], 4),
             "restore_s_first": round(restore[0], 4), "restore_s": round(med, 4),
             "restore_GBps": round((attn + snap) / med / 1e9, 3), "tier_index": tier_out["index"],
@@ -834,13 +837,14 @@ def main():
         print(json.dumps(res), flush=True)
         sys.exit(0 if res_ok else 1)
     if args.paper_hybrid_server:
-        paper_hybrid_server(kvx, args.paper_hybrid_server, args.mode)
+        paper_hybrid_server(kvx, args.paper_hybrid_server, args.mode, args.tier_load_mode)
         return
     if args.paper_hybrid_store:
         paper_hybrid_store(torch, harness, hg, kvx, args.paper_hybrid_store, dev)
         return
     if args.paper_hybrid_only:
-        res, res_ok = paper_hybrid_leg(np, torch, harness, hg, kvx, "zero_copy", dev)
+        # Staged stores and zero-copy loads: the faster mode of each direction across processes.
+        res, res_ok = paper_hybrid_leg(np, torch, harness, hg, kvx, "staged", dev, load_mode="zero_copy")
         print(json.dumps(res), flush=True)
         sys.exit(0 if res_ok else 1)
     if args.tier_server:

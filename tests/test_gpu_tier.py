@@ -96,7 +96,7 @@ def _serving(tier):
         raise
 
 
-@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+@pytest.mark.parametrize("mode", ["zero_copy", "staged", "staged+zero_copy"])
 def test_two_replica_processes_share_one_pool(mode, tmp_path):
     lay = TINY
     n = 3 * lay.C + 100
@@ -299,7 +299,7 @@ def test_prefix_eviction_under_a_small_pool(tmp_path):
     assert "'evictions': 2" in out
 
 
-@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+@pytest.mark.parametrize("mode", ["zero_copy", "staged", "staged+zero_copy"])
 def test_hybrid_prefix_aligned_recovery_across_processes(mode, tmp_path):
     """The paper's hybrid case through the tier (Sec. 2.2): replica A stores a prompt's whole
     chunks plus the recurrent snapshot at its last whole-chunk boundary.  Replica B restores the

@@ -32,9 +32,18 @@ from paper_2609_15021_amd import kvx  # noqa: E402
 POOL_SENT = 0xA5
 
 
+def _pool(lay, slots, mode, **kw):
+    """mode: zero_copy, staged, or staged+zero_copy (staged stores, zero-copy loads)."""
+    store_mode, _, load_mode = mode.partition("+")
+    pool = kvx.kv_pool_create(lay, slots, store_mode, staging_slots=2, chunks_per_batch=2, **kw)
+    if load_mode:
+        kvx.kv_pool_set_modes(pool, store_mode, load_mode)
+    return pool
+
+
 def tier(sock, L, H, D, E, BS, C, slots, mode, nconn, dump):
     lay = kvx.make_layout(L, H, D, E, BS, C)
-    pool = kvx.kv_pool_create(lay, slots, mode, staging_slots=2, chunks_per_batch=2)
+    pool = _pool(lay, slots, mode)
     view = kvx.pool_view(pool)
     view[:] = POOL_SENT
     srv = socket.socket(socket.AF_UNIX, socket.SOCK_STREAM)
@@ -73,8 +82,7 @@ def state_pages(seed, G, npages, pb):
 
 def tier_native(sock, L, H, D, E, BS, C, slots, mode, nconn, dump, index_slots, state_slots=0, state_bytes=0):
     lay = kvx.make_layout(L, H, D, E, BS, C)
-    pool = kvx.kv_pool_create(lay, slots, mode, staging_slots=2, chunks_per_batch=2, num_state_slots=state_slots,
-                              state_slot_bytes=state_bytes)
+    pool = _pool(lay, slots, mode, num_state_slots=state_slots, state_slot_bytes=state_bytes)
     view = kvx.pool_view(pool)
     view[:] = POOL_SENT
     index = kvx.kv_index_create(C, index_slots, state_slots) if index_slots else None

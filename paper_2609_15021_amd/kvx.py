@@ -156,7 +156,8 @@ def _open():
 _lib = _open()
 
 EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slot", "kv_pool_slot_bytes",
-           "kv_pool_num_slots", "kv_pool_set_mode", "kv_pool_set_modes", "kv_pool_async_error", "kv_pool_kernel_stats", "kv_check",
+           "kv_pool_num_slots", "kv_pool_set_mode", "kv_pool_set_modes", "kv_pool_async_error",
+           "kv_pool_kernel_stats", "kv_check",
            "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version", "kv_pool_state_slot",
            "kv_check_state", "kv_store_state", "kv_load_state", "kv_index_create", "kv_index_destroy",
            "kv_index_keys", "kv_index_lookup", "kv_index_unpin", "kv_index_reserve", "kv_index_commit",
@@ -396,6 +397,22 @@ def _block_table_ptr(block_table, cache: Cache):
     return ctypes.c_void_p(block_table.data_ptr())
 
 
+def _in_use_on(t: torch.Tensor, stream) -> None:
+    """The C ABI reads the block table from `stream` until the call's work completes there.  For a
+    stream torch owns (the current stream or a torch.cuda.Stream it created), tell torch's caching
+    allocator, so that a temporary table's memory is not handed out again (and overwritten from
+    another stream) before that.  The allocator records an event on that stream when it frees the
+    table, so a caller's own stream (a raw handle or an ExternalStream), which the caller may
+    destroy first, is left out: there the caller keeps the table alive, as the C ABI requires."""
+    if stream is None:
+        s = torch.cuda.current_stream()
+    elif isinstance(stream, torch.cuda.Stream) and not isinstance(stream, torch.cuda.ExternalStream):
+        s = stream
+    else:
+        return
+    t.record_stream(s)
+
+
 def kv_check(cache: Cache, pool_layout: KvLayout, pool_slots: int, n_tokens: int, chunk_ids, for_store: bool) -> int:
     ids, ptr = _chunk_ids(chunk_ids) if chunk_ids is not None else (None, None)
     return int(_lib.kv_check(ctypes.byref(cache.struct), ctypes.byref(pool_layout), int(pool_slots), int(n_tokens),
@@ -406,12 +423,16 @@ def kv_store(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, st
     ids, ptr = _chunk_ids(chunk_ids)
     _raise(_lib.kv_store(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
                          pool.handle, ptr, _stream_handle(stream)))
+    if block_table is not None and int(n_tokens) > 0:
+        _in_use_on(block_table, stream)
 
 
 def kv_load(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, stream=None) -> None:
     ids, ptr = _chunk_ids(chunk_ids)
     _raise(_lib.kv_load(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
                         pool.handle, ptr, _stream_handle(stream)))
+    if block_table is not None and int(n_tokens) > 0:
+        _in_use_on(block_table, stream)
 
 
 # ---- Pool index (host only) --------------------------------------------------------------

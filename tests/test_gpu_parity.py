@@ -211,6 +211,34 @@ def test_out_of_range_block_is_flagged_and_skipped(mode):
     kvx.kv_pool_destroy(pool)
 
 
+def _explain_slabs(lay, A, bt, n, cid, view, tA, tB, btB):
+    """On a wrong pool: for each wrong (chunk, layer, K/V, block) slab, which source block's bytes it
+    holds (the block-table entry the store effectively used) and the launch's workgroup id of that
+    slab (XCD = id mod 8); and the tables as they read back now."""
+    bpc, rows = lay.C // lay.BS, lay.H * lay.D * lay.E
+    src = A.view(np.uint8).reshape(lay.L, A.shape[1], 2, lay.H, lay.BS, lay.D * lay.E)
+    out = []
+    for i in range(lay.nc(n)):
+        r = min(lay.C, n - i * lay.C)
+        base = int(cid[i]) * lay.slot_bytes
+        for l in range(lay.L):
+            for kv in range(2):
+                plane = base + (l * 2 + kv) * r * rows
+                for j in range(-(-r // lay.BS)):
+                    bs = min(lay.BS, r - j * lay.BS)
+                    got = view[plane + j * lay.BS * rows:plane + (j * lay.BS + bs) * rows]
+                    want_b = int(bt[i * bpc + j])
+                    as_rows = lambda b: src[l, b, kv, :, :bs, :].transpose(1, 0, 2).reshape(-1)
+                    if np.array_equal(got, as_rows(want_b)):
+                        continue
+                    seen = [b for b in range(A.shape[1]) if np.array_equal(got, as_rows(b))]
+                    wg = ((i * lay.L + l) * 2 + kv) * bpc + j
+                    out.append(f"(c{i} l{l} kv{kv} j{j} wg{wg} xcd{wg % 8}: want block {want_b}, got {seen[:2]})")
+    ta, tb = tA.cpu().numpy(), tB.cpu().numpy()
+    return (f"{len(out)} wrong slabs: " + " ".join(out[:24]) +
+            f"; table A intact now: {np.array_equal(ta, bt)}; table B intact now: {np.array_equal(tb, btB)}")
+
+
 @pytest.mark.parametrize("mode", ["zero_copy", "staged"])
 @pytest.mark.parametrize("dims", [(2, 2, 64, 2, 16, 256), (70, 1, 8, 2, 16, 256)], ids=["tiny", "70-layers"])
 def test_per_layer_allocations(mode, dims):
@@ -232,19 +260,54 @@ def test_per_layer_allocations(mode, dims):
     lb = [torch.empty((NB, 2, lay.H, lay.BS, lay.D), dtype=TORCH_INT[lay.E], device=DEV) for _ in range(lay.L)]
     for t in lb:
         t.view(torch.uint8).fill_(CACHE_SENT)
+    tA, tB = bt_tensor(btA), bt_tensor(btB)  # valid until the calls complete on s (the ABI's rule)
     s = torch.cuda.Stream()
     torch.cuda.synchronize()
-    kvx.kv_store(kvx.Cache(la, lay.kv, NB), bt_tensor(btA), n, pool, cid, s)
-    kvx.kv_load(kvx.Cache(lb, lay.kv, NB), bt_tensor(btB), n, pool, cid, s)
+    assert np.array_equal(tA.cpu().numpy(), btA) and np.array_equal(tB.cpu().numpy(), btB)
+    kvx.kv_store(kvx.Cache(la, lay.kv, NB), tA, n, pool, cid, s)
+    kvx.kv_load(kvx.Cache(lb, lay.kv, NB), tB, n, pool, cid, s)
     s.synchronize()
     want_pool = oracle_pool(lay, A, btA, n, cid, nc + 1, POOL_SENT)
-    assert np.array_equal(view, want_pool), "pool: " + first_mismatch(view, want_pool)
+    assert np.array_equal(view, want_pool), ("pool: " + first_mismatch(view, want_pool) + "; " +
+                                             _explain_slabs(lay, A, btA, n, cid, view, tA, tB, btB))
     B0 = np.full(A.shape, 0, dtype=A.dtype)
     B0.view(np.uint8)[:] = CACHE_SENT
     want_B = oracle_unpack_into(lay, B0, btB, n, want_pool, cid)
     got_B = torch.stack(lb).cpu().numpy().view(A.dtype).reshape(A.shape)
     assert np.array_equal(got_B, want_B), "cache B: " + first_mismatch(got_B, want_B)
+    # The library never writes a block table.
+    assert np.array_equal(tA.cpu().numpy(), btA) and np.array_equal(tB.cpu().numpy(), btB)
     assert kvx.kv_pool_async_error(pool) == 0
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_binding_keeps_a_temporary_block_table_until_the_stream_used_it(mode):
+    """Python callers may pass a temporary block table: the binding records it as in use on the
+    call's stream, so torch's caching allocator does not hand its memory to the next tensor (here
+    another table of the same size, uploaded on the default stream) while the call's kernels on
+    another stream have yet to read it.  Without that, the store reads the other table's entries.
+    The producer stream starts behind a 20 ms spin so the kernels run well after the upload."""
+    lay = TINY
+    NB, n = 512, 4096 + 192
+    seed = harness.sub_seed("parity", "temporary-table", mode)
+    A = host_cache(lay, NB, seed, "raw")
+    nblk, nc = lay.nblk(n), lay.nc(n)
+    btA, btX = harness.block_table(seed + 1, NB, nblk), harness.block_table(seed + 2, NB, nblk)
+    cid = harness.chunk_ids(nc, nc, seed + 3)
+    pool = kvx.kv_pool_create(lay.kv, nc, mode, staging_slots=2, chunks_per_batch=2)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    dA = to_device(A)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    hg.spin(20.0, s)
+    kvx.kv_store(kvx.Cache(dA, lay.kv, NB), bt_tensor(btA), n, pool, cid, s)  # the table is dropped here
+    other = bt_tensor(btX)  # same size: the allocator's first candidate for the freed block
+    s.synchronize()
+    del other
+    want = oracle_pool(lay, A, btA, n, cid, nc, POOL_SENT)
+    assert np.array_equal(view, want), "pool: " + first_mismatch(view, want)
     kvx.kv_pool_destroy(pool)
 
 

@@ -203,3 +203,16 @@ def test_native_caller_links_against_the_library(tmp_path):
     r = subprocess.run([build.NATIVE_BIN, "staged", "2", "2", "64", "2", "16", "256", "8", "16", "1", str(tmp_path)],
                        capture_output=True, text=True, timeout=60)
     assert r.returncode == 1 and "cannot read the inputs" in r.stderr, r.stderr
+
+
+def test_null_handles_are_rejected_without_a_gpu():
+    """Entry points given a NULL pool or index return KV_EINVAL with a message (no GPU is touched)."""
+    from paper_2609_15021_amd import kvx
+    lib = kvx._lib
+    assert lib.kv_pool_set_modes(None, kvx.KV_MODE_STAGED, kvx.KV_MODE_ZERO_COPY) == kvx.KV_EINVAL
+    assert b"pool" in lib.kv_last_error()
+    assert lib.kv_pool_set_mode(None, kvx.KV_MODE_STAGED) == kvx.KV_EINVAL
+    assert lib.kv_pool_destroy(None) == kvx.KV_OK   # destroying NULL is a no-op
+    assert lib.kv_store(None, None, 16, None, None, None) == kvx.KV_EINVAL
+    assert lib.kv_load(None, None, 16, None, None, None) == kvx.KV_EINVAL
+    assert lib.kv_index_get_stats(None, None) == kvx.KV_EINVAL

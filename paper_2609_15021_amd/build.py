@@ -86,8 +86,23 @@ def build_native_caller(verbose: bool = False) -> str:
     return NATIVE_BIN
 
 
+TIERD_SRC = os.path.join(CSRC, "kvx_tierd.cpp")
+TIERD_BIN = os.path.join(PKG, "kvx_tierd")
+
+
+def build_tierd(verbose: bool = False) -> str:
+    """The standalone tier daemon: a host program over the C ABI (no kernels of its own)."""
+    tmp = TIERD_BIN + ".tmp"
+    # libkvx.so and the HIP runtime are loaded at run time (dlopen), in that order reversed: the
+    # runtime named on the command line first, so that the library binds to it.
+    _run(["g++", "-std=c++17", "-O2", "-Wall", "-Wextra", "-Werror", "-I", INCLUDE, TIERD_SRC, "-o", tmp,
+          "-Wl,-rpath,/opt/rocm/lib", "-ldl"], verbose)
+    os.replace(tmp, TIERD_BIN)
+    return TIERD_BIN
+
+
 def build_all(verbose: bool = False):
-    return build_kvx(verbose), build_harness(verbose), build_native_caller(verbose)
+    return build_kvx(verbose), build_harness(verbose), build_native_caller(verbose), build_tierd(verbose)
 
 
 if __name__ == "__main__":

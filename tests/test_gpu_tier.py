@@ -8,6 +8,7 @@ The pool bytes (dumped by the tier) and B's cache are compared with the oracle.
 import contextlib
 import gc
 import os
+import signal
 import socket
 import struct
 import subprocess
@@ -272,6 +273,84 @@ def test_prefix_store_and_external_hit(mode, tmp_path):
     got = got_B.numpy().view(A.dtype).reshape(A.shape)
     assert np.array_equal(got, want_B), first_mismatch(got, want_B)
     assert "'entries': 5" in out and "'evictions': 0" in out
+
+
+def _start_daemon(sock, lay, slots, mode, extra=()):
+    from paper_2609_15021_amd import build
+    assert os.path.exists(build.TIERD_BIN), "kvx_tierd not built; run __graft_entry__.build()"
+    # The replicas here are torch processes: the daemon must run the HIP runtime torch ships, or
+    # their IPC handles do not open in it.
+    runtime = os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so")
+    p = subprocess.Popen([build.TIERD_BIN, "--socket", sock, "--layout", ",".join(_dims(lay)), "--slots", str(slots),
+                          "--mode", mode, "--staging-slots", "2", "--chunks-per-batch", "2", "--hip-runtime", runtime,
+                          *extra],
+                         stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    seen, t0 = [], time.time()
+    while time.time() - t0 < 90:
+        line = p.stdout.readline()
+        if line.startswith("READY"):
+            return p
+        if not line and p.poll() is not None:
+            break
+        seen.append(line)
+    p.kill()
+    raise AssertionError(f"kvx_tierd did not start: {''.join(seen)[-2000:]}{p.stdout.read()[-2000:]}")
+
+
+@pytest.mark.parametrize("mode", ["staged+zero_copy", "zero_copy"])
+def test_tier_daemon_serves_a_prefix_cache(mode, tmp_path):
+    """The standalone tier daemon (kvx_tierd: a native program over the C ABI) owns the pool and its
+    index: replica A (a process) stores a prompt through it, replica B gets the whole-chunk hit; the
+    pool the daemon dumps and B's cache equal the oracle's bytes."""
+    lay = TINY
+    n = 5 * lay.C + 100
+    NB = lay.nblk(n) + 9
+    seed, salt = harness.sub_seed("daemon", mode), 13
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.bin")
+    d = _start_daemon(sock, lay, 8, mode, ("--index-slots", "8", "--connections", "2", "--fill", str(POOL_SENT),
+                                           "--dump", dump))
+    with _serving(d):
+        r = subprocess.run([sys.executable, "-u", ROLES, "store-prefix", sock, *_dims(lay), str(NB), str(n), str(seed),
+                            str(salt)], capture_output=True, text=True, timeout=120)
+        assert r.returncode == 0 and "STORED 5" in r.stdout, (r.stdout + r.stderr)[-3000:]
+        tokens = harness.prompt_tokens(seed, n)
+        btB = harness.block_table(seed + 2, NB, lay.nblk(n))
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV)
+        torch.cuda.synchronize()
+        c = _connect(sock)
+        hit = kvx.kv_tier_load_prefix(c.fileno(), kvx.Cache(dB, lay.kv, NB), btB, salt, tokens)
+        got_B = dB.cpu()
+        c.close()
+        out, _ = d.communicate(timeout=90)
+    assert d.returncode == 0 and "TIER ok" in out, out[-2000:]
+    assert "entries=5 pending=0" in out, out[-2000:]
+    assert hit == 5 * lay.C
+    A = host_cache(lay, NB, seed, "raw")
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+    pool = np.fromfile(dump, dtype=np.uint8)
+    want_pool = oracle_pool(lay, A, btA, hit, np.arange(5), 8, POOL_SENT)
+    assert np.array_equal(pool, want_pool), first_mismatch(pool, want_pool)
+    want_B = oracle_unpack_into(lay, np.zeros_like(A), btB, hit, want_pool, np.arange(5))
+    got = got_B.numpy().view(A.dtype).reshape(A.shape)
+    assert np.array_equal(got, want_B), first_mismatch(got, want_B)
+
+
+def test_tier_daemon_stops_cleanly_on_sigterm(tmp_path):
+    """Serving without a connection limit, the daemon stops on SIGTERM: it stops accepting, reports
+    the index and exits 0, removing its socket."""
+    sock = str(tmp_path / "tier.sock")
+    d = _start_daemon(sock, TINY, 4, "staged", ("--connections", "0"))
+    c = _connect(sock)  # an idle replica connection that ends before the signal
+    c.close()
+    time.sleep(0.5)
+    d.send_signal(signal.SIGTERM)
+    try:
+        out, _ = d.communicate(timeout=60)
+    except subprocess.TimeoutExpired:
+        d.kill()
+        raise
+    assert d.returncode == 0 and "TIER ok" in out and "STATS entries=0" in out, out[-2000:]
+    assert not os.path.exists(sock)
 
 
 def test_prefix_eviction_under_a_small_pool(tmp_path):

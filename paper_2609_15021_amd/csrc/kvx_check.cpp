@@ -133,7 +133,8 @@ kv_status check_request(const kv_cache *cache, const kv_layout *pool_layout, int
         seen.reserve(static_cast<size_t>(nc) * 2);
         for (int64_t i = 0; i < nc; ++i)
             if (!seen.insert(chunk_ids[i]).second)
-                return fail(KV_EINVAL, "chunk id %lld appears twice in one store", static_cast<long long>(chunk_ids[i]));
+                return fail(KV_EINVAL, "chunk id %lld appears twice in one store",
+                            static_cast<long long>(chunk_ids[i]));
     }
     return KV_OK;
 }

@@ -481,7 +481,8 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
         if (st != KV_OK)
             return st;
         if (num_slots <= 0 || num_slots > INT32_MAX)
-            return kvx::fail(KV_EINVAL, "num_slots must be in [1, 2^31-1] (got %lld)", static_cast<long long>(num_slots));
+            return kvx::fail(KV_EINVAL, "num_slots must be in [1, 2^31-1] (got %lld)",
+                             static_cast<long long>(num_slots));
         if (opts->mode != KV_MODE_ZERO_COPY && opts->mode != KV_MODE_STAGED)
             return kvx::fail(KV_EINVAL, "opts->mode must be KV_MODE_ZERO_COPY or KV_MODE_STAGED (got %u)", opts->mode);
         if (opts->host_kind != KV_HOST_COHERENT && opts->host_kind != KV_HOST_NONCOHERENT)
@@ -503,7 +504,8 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
         if (opts->num_state_slots < 0 || opts->state_slot_bytes < 0 ||
             (opts->num_state_slots > 0) != (opts->state_slot_bytes > 0))
             return kvx::fail(KV_EINVAL, "num_state_slots (%lld) and state_slot_bytes (%lld) must both be 0 or both > 0",
-                             static_cast<long long>(opts->num_state_slots), static_cast<long long>(opts->state_slot_bytes));
+                             static_cast<long long>(opts->num_state_slots),
+                             static_cast<long long>(opts->state_slot_bytes));
         if (opts->state_slot_bytes % 16 != 0)
             return kvx::fail(KV_EUNSUPPORTED, "state_slot_bytes %lld is not a multiple of 16",
                              static_cast<long long>(opts->state_slot_bytes));
@@ -549,7 +551,8 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
             // One pinned, mapped region of exactly region_bytes (Sec. 3.3: no rounding allocator,
             // and never a silent fallback to pageable memory).
             const unsigned flags = hipHostMallocMapped | hipHostMallocPortable |
-                                   (p->host_kind == KV_HOST_COHERENT ? hipHostMallocCoherent : hipHostMallocNonCoherent);
+                                   (p->host_kind == KV_HOST_COHERENT ? hipHostMallocCoherent
+                                                                     : hipHostMallocNonCoherent);
             const auto t0 = std::chrono::steady_clock::now();
             void *host = nullptr;
             e = hipHostMalloc(&host, static_cast<size_t>(region_bytes), flags);
@@ -578,7 +581,8 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
                 return bail(kvx::hip_fail(e, "hipHostGetDevicePointer(pool)", __FILE__, __LINE__));
             p->dev_base = static_cast<uint8_t *>(dptr);
 
-            e = hipHostMalloc(reinterpret_cast<void **>(&p->err_host), 256, hipHostMallocMapped | hipHostMallocCoherent);
+            e = hipHostMalloc(reinterpret_cast<void **>(&p->err_host), 256,
+                              hipHostMallocMapped | hipHostMallocCoherent);
             if (e != hipSuccess)
                 return bail(kvx::hip_fail(e, "hipHostMalloc(err)", __FILE__, __LINE__));
             std::memset(p->err_host, 0, 256);
@@ -594,7 +598,8 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
                 // Physically contiguous staging: the DMA engines read and write it, and staging placed in
                 // fragmented (recycled) device memory was measured to slow D2H copies by ~5%.  If the
                 // runtime refuses the flag, plain device memory is used and kv_pool_info reports it.
-                e = hipExtMallocWithFlags(reinterpret_cast<void **>(&p->staging), staging_bytes, hipDeviceMallocContiguous);
+                e = hipExtMallocWithFlags(reinterpret_cast<void **>(&p->staging), staging_bytes,
+                                          hipDeviceMallocContiguous);
                 p->staging_contiguous = e == hipSuccess;
                 if (e != hipSuccess) {
                     (void)hipGetLastError();

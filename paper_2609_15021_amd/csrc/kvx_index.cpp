@@ -242,7 +242,8 @@ kv_status kv_index_create(int32_t chunk_tokens, int64_t num_slots, int64_t num_s
             return kvx::fail(KV_EINVAL, "out must not be NULL");
         *out = nullptr;
         if (chunk_tokens < 1 || num_slots < 1 || num_state_slots < 0)
-            return kvx::fail(KV_EINVAL, "need chunk_tokens >= 1, num_slots >= 1, num_state_slots >= 0 (got %d, %lld, %lld)",
+            return kvx::fail(KV_EINVAL,
+                             "need chunk_tokens >= 1, num_slots >= 1, num_state_slots >= 0 (got %d, %lld, %lld)",
                              chunk_tokens, static_cast<long long>(num_slots), static_cast<long long>(num_state_slots));
         std::unique_ptr<kv_index> x(new kv_index());  // freed if a container below throws
         x->C = chunk_tokens;

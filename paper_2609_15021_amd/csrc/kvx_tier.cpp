@@ -142,7 +142,8 @@ class Connection {
                 h.state_layers < 0 || h.state_layers > kMaxLayers || h.n_table > kMaxPayload ||
                 h.n_chunks > kMaxPayload || h.n_ids > kMaxPayload)
                 return kvx::fail(KV_EINVAL, "tier: malformed request header");
-            const int64_t payload = static_cast<int64_t>(h.num_layers + h.state_layers) * int64_t(sizeof(kv_ipc_buffer)) +
+            const int64_t payload = static_cast<int64_t>(h.num_layers + h.state_layers) *
+                                        int64_t(sizeof(kv_ipc_buffer)) +
                                     h.n_table * int64_t(sizeof(int32_t)) + h.n_chunks * int64_t(sizeof(int64_t)) +
                                     h.n_ids * int64_t(sizeof(int32_t));
             if (payload > kMaxPayload)
@@ -636,16 +637,16 @@ kv_status kv_tier_run(kv_pool *pool, kv_index *index, int listen_fd, int32_t con
 kv_status kv_tier_store(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                         const int64_t *chunk_ids, void *stream) {
     return kvx::guarded([&]() -> kv_status {
-        return send_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream, nullptr,
-                            nullptr);
+        return send_request(kOpStore, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream,
+                            nullptr, nullptr);
     });
 }
 
 kv_status kv_tier_load(int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                        const int64_t *chunk_ids, void *stream) {
     return kvx::guarded([&]() -> kv_status {
-        return send_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream, nullptr,
-                            nullptr);
+        return send_request(kOpLoad, fd, cache, block_table, n_tokens, chunk_ids, 0, nullptr, nullptr, 0, stream,
+                            nullptr, nullptr);
     });
 }
 
@@ -654,8 +655,8 @@ kv_status kv_tier_store_prefix(int fd, const kv_cache *cache, const int32_t *blo
                                int64_t *stored_chunks, int32_t *stored_state, void *stream) {
     return kvx::guarded([&]() -> kv_status {
         int64_t v = 0, v2 = 0;
-        const kv_status st = send_request(kOpStorePrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens, state,
-                                          state_page, stream, &v, &v2);
+        const kv_status st = send_request(kOpStorePrefix, fd, cache, block_table, n_tokens, nullptr, salt, tokens,
+                                          state, state_page, stream, &v, &v2);
         if (stored_chunks)
             *stored_chunks = st == KV_OK ? v : 0;
         if (stored_state)

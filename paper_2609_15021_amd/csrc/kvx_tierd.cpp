@@ -73,7 +73,8 @@ bool load_api(const std::string &hip_runtime, Api *api) {
         std::fprintf(stderr, "kvx_tierd: cannot load %s/libkvx.so: %s\n", dir.c_str(), dlerror());
         return false;
     }
-    return resolve(lib, "kv_pool_create", &api->pool_create) && resolve(lib, "kv_pool_set_modes", &api->pool_set_modes) &&
+    return resolve(lib, "kv_pool_create", &api->pool_create) &&
+           resolve(lib, "kv_pool_set_modes", &api->pool_set_modes) &&
            resolve(lib, "kv_pool_slot", &api->pool_slot) && resolve(lib, "kv_pool_slot_bytes", &api->pool_slot_bytes) &&
            resolve(lib, "kv_pool_destroy", &api->pool_destroy) && resolve(lib, "kv_index_create", &api->index_create) &&
            resolve(lib, "kv_index_get_stats", &api->index_get_stats) &&

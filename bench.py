@@ -1026,6 +1026,16 @@ def main():
     both = concurrent_leg(torch, kvx, rep_a, rep_b, t_a, t_b, n, ids, pool)
     log(f"[bench] store and load at once ({both['bytes_per_direction'] / 2**30:.0f} GiB each): "
         f"{both['aggregate_GBps']} GB/s in total (store {both['store_GBps']}, load {both['load_GBps']} GB/s)")
+    # The same with staged stores and zero-copy loads: the load's kernels read the pool over the
+    # link on the caller's stream while the store's copies run on the side streams, so the two
+    # directions need not take turns on the side streams.
+    if args.mode == "staged" and info["staging_bytes"]:
+        kvx.kv_pool_set_modes(pool, "staged", "zero_copy")
+        both["staged_store_zero_copy_load"] = concurrent_leg(torch, kvx, rep_a, rep_b, t_a, t_b, n, ids, pool)
+        kvx.kv_pool_set_modes(pool, args.mode, args.mode)
+        mixed = both["staged_store_zero_copy_load"]
+        log(f"[bench] store and load at once, staged stores and zero-copy loads: {mixed['aggregate_GBps']} GB/s "
+            f"in total (store {mixed['store_GBps']}, load {mixed['load_GBps']} GB/s)")
 
     zc = None
     if not args.no_zero_copy_compare:

@@ -1,6 +1,6 @@
 // Pack (store) and unpack (load) kernels for gfx950.
 //
-// One workgroup moves one slab: the (layer l, K/V, block j) piece of chunk i, i.e. the
+// A workgroup moves one slab at a time: the (layer l, K/V, block j) piece of chunk i, i.e. the
 // bs <= BS tokens of one paged block for one layer and one of K/V.  On the cache side the
 // slab is the contiguous [H][BS][D] region of that block (HND, the paper's replica layout,
 // Table 1); on the chunk side it is the contiguous [bs][H][D] run of token-major rows
@@ -20,8 +20,12 @@
 // and subnormals survive).
 //
 // Index math is one division at thread start; afterwards every step is an addition with
-// carry.  Streaming data is read and written nontemporally; device-side launches cap
-// residency at 4 workgroups per CU (see KVX_LDS_RESERVE).
+// carry.  Streaming data is read and written nontemporally.  Device-side (staged) launches
+// run one workgroup per slab and cap residency at 4 workgroups per CU (KVX_LDS_RESERVE).
+// Host-side (zero-copy) launches run a few dozen workgroups that stride over the slabs
+// (KVX_HOST_WGS_*): the link bounds them, and the rest of the chip stays free.
+#include <algorithm>
+
 #include "kvx_internal.h"
 
 namespace kvx {
@@ -49,6 +53,17 @@ typedef uint32_t vec16 __attribute__((ext_vector_type(4)));
 // fewer concurrent 32 KiB streams per CU keep the HBM read/write mix efficient.
 #ifndef KVX_LDS_RESERVE
 #define KVX_LDS_RESERVE 40960
+#endif
+// Workgroups of a host-side (zero-copy) pack / unpack launch; each strides over the
+// launch's slabs (0: one workgroup per slab).  Measured on MI355X at the 27B-class layout
+// (one workgroup per slab: store 54.5, load 55.9 GB/s): 64 for pack gives 55.9 GB/s (16:
+// 49.8, 256: 54.7); 32 for unpack gives 57.0 GB/s (16: 44, 64 to 256: 57.5) and, with
+// a staged store running at the same time, lets both directions share the link.
+#ifndef KVX_HOST_WGS_PACK
+#define KVX_HOST_WGS_PACK 64
+#endif
+#ifndef KVX_HOST_WGS_UNPACK
+#define KVX_HOST_WGS_UNPACK 32
 #endif
 
 __device__ __forceinline__ vec16 load16(const vec16 *p) {
@@ -112,19 +127,31 @@ __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, in
 
 // HOST_SIDE marks launches whose chunk side is mapped pinned host memory (zero-copy mode);
 // the body is the same, the instantiation (and launch occupancy) is separate.
-template <int DIR, int U, bool HOST_SIDE>
-__global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
-    // Workgroup -> (chunk c, layer ll, kv, block j); j varies fastest so consecutive
-    // workgroups touch consecutive chunk-side regions.
+template <int DIR, int U>
+__device__ __forceinline__ void move_slab_id(const GatherArgs &a, int64_t id) {
+    // Slab id -> (chunk c, layer ll, kv, block j); j varies fastest so consecutive ids
+    // touch consecutive chunk-side regions.
     const int bpc = a.blocks_per_chunk;
-    const int64_t wg = blockIdx.x;
-    const int j = static_cast<int>(wg % bpc);
-    int64_t rest = wg / bpc;
+    const int j = static_cast<int>(id % bpc);
+    int64_t rest = id / bpc;
     const int kv = static_cast<int>(rest & 1);
     rest >>= 1;
     const int ll = static_cast<int>(rest % a.nlayers);
     const int c = static_cast<int>(rest / a.nlayers);
     move_slab<DIR, U>(a, c, ll, kv, j);
+}
+
+template <int DIR, int U, bool HOST_SIDE>
+__global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
+    if constexpr (HOST_SIDE) {
+        // A capped grid strides over the slabs: the link, not the number of waves in flight,
+        // bounds these launches, and the CUs they leave free run other streams' kernels.
+        const int64_t total = static_cast<int64_t>(a.nchunks) * a.nlayers * 2 * a.blocks_per_chunk;
+        for (int64_t id = blockIdx.x; id < total; id += gridDim.x)
+            move_slab_id<DIR, U>(a, id);
+    } else {
+        move_slab_id<DIR, U>(a, blockIdx.x);  // one workgroup per slab
+    }
 }
 
 template <int DIR, int U>
@@ -228,9 +255,11 @@ int max_chunks_per_launch(const Geometry &g, int nlayers) {
 }
 
 hipError_t launch_gather(const GatherArgs &args, Direction dir, bool host_side, hipStream_t stream) {
-    const int64_t grid = static_cast<int64_t>(args.nchunks) * args.nlayers * 2 * args.blocks_per_chunk;
-    if (grid <= 0)
+    const int64_t slabs = static_cast<int64_t>(args.nchunks) * args.nlayers * 2 * args.blocks_per_chunk;
+    if (slabs <= 0)
         return hipSuccess;
+    const int64_t host_wgs = dir == kPack ? KVX_HOST_WGS_PACK : KVX_HOST_WGS_UNPACK;
+    const int64_t grid = host_side && host_wgs > 0 ? std::min<int64_t>(slabs, host_wgs) : slabs;
     const void *fn;
     if (host_side)
         fn = dir == kPack ? reinterpret_cast<const void *>(&gather_kernel<kPack, kUnroll, true>)

@@ -72,6 +72,7 @@ struct StateArgs {
     uint8_t *base;                     // device-visible packed side (state pool or staging)
     int64_t page_stride, page_bytes, piece;
     int64_t q0;
+    int64_t npieces;  // pieces in this launch (set by launch_state)
     int32_t G, ppp, nsnap, pad;
     int64_t page[kMaxLaunchSnapshots];  // device page id of each snapshot
     int64_t off[kMaxLaunchSnapshots];   // byte offset at `base` of each snapshot's packed bytes

@@ -54,6 +54,7 @@ def parse():
     ap.add_argument("--pool-blocks", type=int, default=10240, help="blocks per cache allocation (160k tokens)")
     ap.add_argument("--no-256k", action="store_true", help="skip the 256k restore measurement")
     ap.add_argument("--no-zero-copy-compare", action="store_true")
+    ap.add_argument("--no-compute-overlap", action="store_true", help="skip the restore-during-GEMMs measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paper-layout", action="store_true", help="skip the paper-native layout measurement")
     ap.add_argument("--paper-layout-only", action="store_true",
@@ -778,6 +779,55 @@ def concurrent_leg(torch, kvx, rep_a, rep_b, t_a, t_b, n, ids, pool, reps=3):
                         "replica B, enqueued together on two streams, disjoint slots"}
 
 
+def compute_overlap_leg(torch, kvx, rep_b, t_b, n, ids, pool, dev, size=8192, reps=3):
+    """A replica restoring a prefix while it computes for other requests: a stream of bf16 GEMMs
+    (size^3, plain 2-D matmuls) runs on one stream while `kv_load` restores the whole prefix on
+    another.  Returns GEMM TFLOP/s and restore seconds, alone and together (medians)."""
+    a = torch.randn(size, size, dtype=torch.bfloat16, device=dev)
+    b = torch.randn(size, size, dtype=torch.bfloat16, device=dev)
+    c = torch.empty(size, size, dtype=torch.bfloat16, device=dev)
+    flop = 2.0 * size ** 3
+    sg, sr = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    def gemms(k):
+        with torch.cuda.stream(sg):
+            for _ in range(k):
+                torch.matmul(a, b, out=c)
+
+    def timed(k, restore):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        w0 = time.perf_counter()
+        if restore:
+            ev[2].record(sr)
+            kvx.kv_load(rep_b.cache, t_b, n, pool, ids, sr)
+            ev[3].record(sr)
+        if k:
+            ev[0].record(sg)
+            gemms(k)
+            ev[1].record(sg)
+        sg.synchronize()
+        sr.synchronize()
+        wall = time.perf_counter() - w0
+        g = ev[0].elapsed_time(ev[1]) / 1e3 if k else None
+        r = ev[2].elapsed_time(ev[3]) / 1e3 if restore else None
+        return g, r, wall
+
+    gemms(5)
+    sg.synchronize()
+    g20 = timed(20, False)[0]
+    r_alone = statistics.median([timed(0, True)[1] for _ in range(reps)])
+    k = max(20, int(round(r_alone / (g20 / 20))))  # GEMMs that take about as long as the restore
+    g_alone = statistics.median([timed(k, False)[0] for _ in range(reps)])
+    both = [timed(k, True) for _ in range(reps)]
+    g_both = statistics.median([x[0] for x in both])
+    r_both = statistics.median([x[1] for x in both])
+    return {"gemm": f"{k} x bf16 matmul {size}x{size}x{size}", "gemm_TFLOPs_alone": round(k * flop / g_alone / 1e12, 1),
+            "gemm_TFLOPs_with_restore": round(k * flop / g_both / 1e12, 1),
+            "restore_s_alone": round(r_alone, 4), "restore_s_with_gemm": round(r_both, 4),
+            "gemm_slowdown": round(g_both / g_alone, 3), "restore_slowdown": round(r_both / r_alone, 3)}
+
+
 def cpu_baseline(np, oracle, n_chunks=64):
     """The oracle timed on host cores: store + load of a bounded sample of the workload."""
     rng = np.random.default_rng(2609)
@@ -1037,6 +1087,19 @@ def main():
         log(f"[bench] store and load at once, staged stores and zero-copy loads: {mixed['aggregate_GBps']} GB/s "
             f"in total (store {mixed['store_GBps']}, load {mixed['load_GBps']} GB/s)")
 
+    # A restore while the replica computes (GEMMs on another stream), per load mode.
+    overlap = None
+    if not args.no_compute_overlap:
+        overlap = {}
+        load_modes = ["staged", "zero_copy"] if info["staging_bytes"] else ["zero_copy"]
+        for lm in load_modes:
+            kvx.kv_pool_set_modes(pool, args.mode, lm)
+            overlap[lm] = compute_overlap_leg(torch, kvx, rep_b, t_b, n, ids, pool, dev)
+            log(f"[bench] restore during GEMMs ({lm} loads): GEMM {overlap[lm]['gemm_TFLOPs_alone']} -> "
+                f"{overlap[lm]['gemm_TFLOPs_with_restore']} TFLOP/s, restore {overlap[lm]['restore_s_alone']} -> "
+                f"{overlap[lm]['restore_s_with_gemm']} s")
+        kvx.kv_pool_set_modes(pool, args.mode, args.mode)
+
     zc = None
     if not args.no_zero_copy_compare:
         other_mode = "zero_copy" if args.mode == "staged" else "staged"
@@ -1160,6 +1223,7 @@ def main():
         "roofline": roof,
         "concurrent_store_load": both,
         "zero_copy_compare": zc,
+        "restore_during_compute": overlap,
         "pool_alloc_s": round(alloc_s, 4),
         "pool_alloc_s_256k": None if alloc_s_256k is None else round(alloc_s_256k, 4),
         "staging_contiguous": bool(staging_contig),

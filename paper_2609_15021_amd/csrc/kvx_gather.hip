@@ -267,8 +267,8 @@ hipError_t launch_gather(const GatherArgs &args, Direction dir, bool host_side, 
     else
         fn = dir == kPack ? reinterpret_cast<const void *>(&gather_kernel<kPack, kUnroll, false>)
                           : reinterpret_cast<const void *>(&gather_kernel<kUnpack, kUnroll, false>);
-    // Device-side (staged) launches cap residency with reserved LDS; host-side launches wait
-    // on PCIe round trips and keep full occupancy.
+    // Device-side (staged) launches cap residency with reserved LDS; host-side launches are
+    // already few workgroups and reserve none.
     const unsigned lds = host_side ? 0u : static_cast<unsigned>(KVX_LDS_RESERVE);
     void *kargs[] = {const_cast<GatherArgs *>(&args)};
     // hipLaunchKernel reports launch failures directly (no sticky last-error state).

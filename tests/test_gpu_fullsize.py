@@ -94,6 +94,49 @@ def test_fullsize_store_load(mode, n, NB):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("mode", ["staged", "zero_copy"])
+def test_fullsize_per_layer_128k(mode):
+    """The benchmark's own configuration: each replica holds its cache as one device allocation
+    per layer (64 tensors of 10,240 blocks), 128k tokens, the pool's default batch and ring.
+    Sampled chunks equal the oracle's bytes; every layer's restored blocks equal the source's;
+    blocks outside B's table stay zero."""
+    lay, n, NB = B27, 131072, 10240
+    nblk, nc = lay.nblk(n), lay.nc(n)
+    seed = harness.sub_seed("fullsize-per-layer", n)
+    print(f"[fullsize] per-layer mode={mode} n={n} NB={NB} nc={nc}", flush=True)
+    per_layer = NB * 2 * lay.H * lay.BS * lay.D  # elements per layer
+    A = [torch.empty((NB, 2, lay.H, lay.BS, lay.D), dtype=torch.int16, device=DEV) for _ in range(lay.L)]
+    B = [torch.zeros_like(t) for t in A]
+    for l, t in enumerate(A):  # the same values as layer l of one [L][NB]... tensor
+        hg.fill_values(t, l * per_layer, seed, "n01", 2)
+    btA = harness.block_table(seed + 1, NB, nblk)
+    btB = harness.block_table(seed + 2, NB, nblk)
+    tA, tB = torch.from_numpy(btA).to(DEV), torch.from_numpy(btB).to(DEV)
+    ids = harness.chunk_ids(nc, nc)
+    pool = kvx.kv_pool_create(lay.kv, nc, mode, staging_slots=3 if mode == "staged" else 0)
+    view = kvx.pool_view(pool)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()  # fills ran on the default stream; s is non-blocking
+    kvx.kv_store(kvx.Cache(A, lay.kv, NB), tA, n, pool, ids, s)
+    kvx.kv_load(kvx.Cache(B, lay.kv, NB), tB, n, pool, ids, s)
+    s.synchronize()
+    assert kvx.kv_pool_async_error(pool) == 0
+    bpc = lay.C // lay.BS
+    for i in sorted({0, nc // 2, nc - 1}):
+        want = _oracle_slot(seed, NB, btA[i * bpc:(i + 1) * bpc], lay.C)
+        assert np.array_equal(view[i * lay.slot_bytes:(i + 1) * lay.slot_bytes], want), \
+            f"chunk {i}: pool differs from the oracle"
+    ta = torch.from_numpy(btA.astype(np.int64)).to(DEV)
+    tb = torch.from_numpy(btB.astype(np.int64)).to(DEV)
+    unused = torch.from_numpy(np.setdiff1d(np.arange(NB), btB)[:256]).to(DEV)
+    for l in range(lay.L):
+        assert torch.equal(A[l][ta], B[l][tb]), f"layer {l}: restored blocks differ from the source"
+        assert not bool(B[l][unused].any()), f"layer {l}: a block outside the table was written"
+    kvx.kv_pool_destroy(pool)
+    del A, B
+    torch.cuda.empty_cache()
+
+
 def test_six_turn_session_with_producer_delays():
     """Initial 128k context, six turns, 2,048 new tokens per later turn; the producer stores only
     its new chunks after a seeded 5-50 ms spin and its own fill on the same stream; the other

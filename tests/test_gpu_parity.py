@@ -163,6 +163,39 @@ def test_load_into_disjoint_blocks_of_same_allocation(mode):
 
 
 @pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_load_with_repeated_chunk_ids(mode):
+    """A load may name one slot for several chunks (they are reads): here slot 2 for chunks 0 and
+    2 of the restored prefix, whose last chunk is partial (100 of 256 tokens, read from a full
+    slot).  Cache B equals the oracle's unpack of the same ids, byte for byte."""
+    lay, NB = TINY, 512
+    seed = harness.sub_seed("parity", "repeated-ids", mode)
+    A = host_cache(lay, NB, seed, "raw")
+    n_s, ids_s = 3 * lay.C + 40, [0, 1, 2, 3]
+    n_l, ids_l = 3 * lay.C + 100, [2, 0, 2, 1]
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n_s))
+    btB = harness.block_table(seed + 2, NB, lay.nblk(n_l))
+    pool = kvx.kv_pool_create(lay.kv, 4, mode, staging_slots=2, chunks_per_batch=2)
+    view = kvx.pool_view(pool)
+    view[:] = POOL_SENT
+    dA, dB = to_device(A), device_cache(lay, NB, fill=CACHE_SENT)
+    tA, tB = bt_tensor(btA), bt_tensor(btB)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    kvx.kv_store(kvx.Cache(dA, lay.kv, NB), tA, n_s, pool, ids_s, s)
+    kvx.kv_load(kvx.Cache(dB, lay.kv, NB), tB, n_l, pool, ids_l, s)
+    s.synchronize()
+    want_pool = oracle_pool(lay, A, btA, n_s, ids_s, 4, POOL_SENT)
+    assert np.array_equal(view, want_pool), "pool: " + first_mismatch(view, want_pool)
+    B0 = np.full_like(A, 0).view(np.uint8)
+    B0[:] = CACHE_SENT
+    want_B = oracle_unpack_into(lay, B0.view(A.dtype).reshape(A.shape), btB, n_l, want_pool, ids_l)
+    got_B = to_host(dB, A)
+    assert np.array_equal(got_B, want_B), "cache B: " + first_mismatch(got_B, want_B)
+    assert kvx.kv_pool_async_error(pool) == 0
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
 def test_zero_tokens_is_noop(mode):
     lay = TINY
     pool = kvx.kv_pool_create(lay.kv, 2, mode)

@@ -240,7 +240,8 @@ KV_API kv_status kv_pool_kernel_stats(kv_pool *pool, int which, int reset, int64
  * layer pointers and chunk_ids, chunk ids in [0, pool_slots), and for a store
  * pairwise distinct (duplicates make the result order dependent).  GPU-path
  * limits give KV_EUNSUPPORTED: D*E % 16 != 0, a layer pointer or
- * block_stride not 16-byte aligned, more than 2^31-1 slots.
+ * block_stride not 16-byte aligned, more than 2^31-1 slots, a block
+ * (2*H*BS*D*E bytes) over 2 GiB.
  * Returns KV_OK / KV_EINVAL / KV_EUNSUPPORTED with kv_last_error set.
  */
 KV_API kv_status kv_check(const kv_cache *cache, const kv_layout *pool_layout, int64_t pool_slots,

@@ -62,10 +62,12 @@ kv_status check_layout(const kv_layout &lay) {
     if (row % 16 != 0)
         return fail(KV_EUNSUPPORTED, "head_dim*elem_bytes = %lld is not a multiple of 16 bytes",
                     static_cast<long long>(row));
-    // Slabs are indexed with 32-bit vector offsets inside one block.
-    const int64_t block_vecs = 2LL * lay.num_kv_heads * lay.block_size * row / 16;
-    if (block_vecs > (int64_t{1} << 30))
-        return fail(KV_EUNSUPPORTED, "block of %lld bytes is too large", static_cast<long long>(block_vecs * 16));
+    // Slabs (one block's K or V) are addressed with signed 32-bit byte offsets: at most 2 GiB
+    // per block.
+    const int64_t block_bytes = 2LL * lay.num_kv_heads * lay.block_size * row;
+    if (block_bytes > (int64_t{1} << 31))
+        return fail(KV_EUNSUPPORTED, "block of %lld bytes is too large (at most 2 GiB)",
+                    static_cast<long long>(block_bytes));
     return KV_OK;
 }
 

@@ -92,6 +92,10 @@ def test_kv_check_rules():
     assert _check(kvx, _fake_cache(kvx, lay, order=kvx.KV_BLOCK_NHD), lay, 4, 10, [0], True) == kvx.KV_OK
     assert _check(kvx, _fake_cache(kvx, lay, order=2), lay, 4, 10, [0], True) == kvx.KV_EINVAL
     assert _check(kvx, _fake_cache(kvx, lay, reserved=1), lay, 4, 10, [0], True) == kvx.KV_EINVAL
+    two_gib = kvx.make_layout(2, 64, 1024, 4, 4096, 4096)                # 2 GiB blocks: the largest allowed
+    assert _check(kvx, _fake_cache(kvx, two_gib, 2), two_gib, 2, 10, [0], True) == kvx.KV_OK
+    four_gib = kvx.make_layout(2, 128, 1024, 4, 4096, 4096)              # slabs past 32-bit byte offsets
+    assert _check(kvx, _fake_cache(kvx, four_gib, 2), four_gib, 2, 10, [0], True) == kvx.KV_EUNSUPPORTED
 
 
 def test_kv_check_agrees_with_oracle_validation():

@@ -3,7 +3,8 @@
 * kv_pool_destroy waits for every store/load still queued on caller streams (they
   write the pool or its staging), so freeing the pool never races with the device.
 * Two host threads, each with its own stream and cache, use one pool at the same
-  time: the pool serialises enqueues and its staging ring stays ordered across streams.
+  time (both storing, or one storing while the other loads): the pool serialises
+  enqueues and its staging ring stays ordered across streams.
 """
 import threading
 import time
@@ -15,7 +16,8 @@ import torch
 import harness
 from harness import gpu as hg
 from paper_2609_15021_amd import kvx
-from tests.gpu_support import TINY, bt_tensor, host_cache, oracle_pool, to_device
+from tests.gpu_support import (TINY, bt_tensor, device_cache, first_mismatch, host_cache, oracle_pool,
+                               oracle_unpack_into, to_device, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -75,6 +77,61 @@ def test_two_threads_share_one_pool(mode):
     assert not errors, errors
     want = oracle_pool(lay, A, bt, n, np.arange(16), 16, 0)
     assert np.array_equal(view, want)
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged", "staged+zero_copy"])
+def test_one_thread_stores_while_another_loads(mode):
+    """Thread 0 stores chunks 0-7 of replica A's prefix again and again while thread 1 restores
+    chunks 8-15 (stored beforehand) into replica B, each on its own stream, through one pool with a
+    two-slot ring of one chunk per batch.  Afterwards the pool and B equal the oracle's bytes."""
+    store_mode, load_mode = (mode.split("+") * 2)[:2]
+    lay, NB, n = TINY, 512, 4096
+    seed = harness.sub_seed("store-while-load", mode)
+    A = host_cache(lay, NB, seed, "raw")
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+    btB = harness.block_table(seed + 2, NB, lay.nblk(n))
+    pool = kvx.kv_pool_create(lay.kv, 16, "staged", staging_slots=2, chunks_per_batch=1)
+    kvx.kv_pool_set_modes(pool, store_mode, load_mode)
+    view = kvx.pool_view(pool)
+    view[:] = 0
+    dA, dB = to_device(A), device_cache(lay, NB, fill=0x5A)
+    cA, cB = kvx.Cache(dA, lay.kv, NB), kvx.Cache(dB, lay.kv, NB)
+    half, hb = n // 2, n // 2 // lay.BS
+    tA_lo, tA_hi, tB_hi = bt_tensor(btA[:hb]), bt_tensor(btA[hb:]), bt_tensor(btB[hb:])
+    torch.cuda.synchronize()
+    kvx.kv_store(cA, tA_hi, half, pool, np.arange(8, 16))  # the chunks thread 1 restores
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    errors = []
+
+    def worker(k):
+        try:
+            for _ in range(8):
+                hg.spin(1.0, streams[k])
+                if k == 0:
+                    kvx.kv_store(cA, tA_lo, half, pool, np.arange(8), streams[0])
+                else:
+                    kvx.kv_load(cB, tB_hi, half, pool, np.arange(8, 16), streams[1])
+            streams[k].synchronize()
+        except Exception as e:  # surfaced below
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in (0, 1)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    want_pool = oracle_pool(lay, A, btA, n, np.arange(16), 16, 0)
+    assert np.array_equal(view, want_pool), "pool: " + first_mismatch(view, want_pool)
+    B0 = np.full_like(A, 0).view(np.uint8)
+    B0[:] = 0x5A
+    want_B = oracle_unpack_into(lay, B0.view(A.dtype).reshape(A.shape), btB[hb:], half, want_pool[8 * lay.slot_bytes:],
+                                np.arange(8))
+    got_B = to_host(dB, A)
+    assert np.array_equal(got_B, want_B), "cache B: " + first_mismatch(got_B, want_B)
+    assert kvx.kv_pool_async_error(pool) == 0
     kvx.kv_pool_destroy(pool)
 
 

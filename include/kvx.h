@@ -153,7 +153,7 @@ typedef struct kv_pool_info {
     int32_t staging_slots;
     int32_t chunks_per_batch;
     int32_t side_streams;
-    int32_t staging_contiguous; /* 1: staging is one physically contiguous device allocation */
+    int32_t staging_contiguous; /* always 0: staging is plain device memory (field kept for layout) */
     void *host_base;           /* host address of slot 0 */
     void *device_base;         /* device address of slot 0 (mapped pinned memory) */
     int64_t num_state_slots;

@@ -595,16 +595,13 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
                 p->cpb = cpb;
                 p->S = S;
                 const size_t staging_bytes = static_cast<size_t>(K) * cpb * static_cast<size_t>(p->geo.slot_bytes);
-                // Physically contiguous staging: the DMA engines read and write it, and staging placed in
-                // fragmented (recycled) device memory was measured to slow D2H copies by ~5%.  If the
-                // runtime refuses the flag, plain device memory is used and kv_pool_info reports it.
-                e = hipExtMallocWithFlags(reinterpret_cast<void **>(&p->staging), staging_bytes,
-                                          hipDeviceMallocContiguous);
-                p->staging_contiguous = e == hipSuccess;
-                if (e != hipSuccess) {
-                    (void)hipGetLastError();
-                    e = hipMalloc(reinterpret_cast<void **>(&p->staging), staging_bytes);
-                }
+                // Plain device memory.  Physically contiguous staging (hipExtMallocWithFlags with
+                // hipDeviceMallocContiguous) was used before, but on MI355X with this runtime, once such
+                // an allocation had been freed, later allocations of the process read and wrote wrong
+                // bytes (156 of 480 seeded round trips in one process); plain staging measured the same
+                // transfer rates.
+                p->staging_contiguous = false;
+                e = hipMalloc(reinterpret_cast<void **>(&p->staging), staging_bytes);
                 if (e != hipSuccess)
                     return bail(kvx::hip_fail(e, "hipMalloc(staging)", __FILE__, __LINE__));
                 for (int s = 0; s < S; ++s) {

@@ -150,7 +150,7 @@ struct kv_pool {
     // Staging ring (staged mode).
     int K = 0, cpb = 0, S = 0;
     uint8_t *staging = nullptr;     // K slots of cpb*slot_bytes each
-    bool staging_contiguous = false;  // physically contiguous allocation granted
+    bool staging_contiguous = false;  // always false: staging is plain device memory
     std::vector<hipStream_t> sides;
     std::vector<hipEvent_t> ev_free;   // staging slot k may be overwritten once this completes
     std::vector<bool> free_recorded;

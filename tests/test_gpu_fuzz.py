@@ -8,9 +8,8 @@ random bytes, one device allocation per layer.  Pool and destination cache must 
 oracle's bytes, sentinels included.  Non-power-of-two head counts and row widths exercise the
 kernels' carry-based index walk; small rings and strided zero-copy grids exercise the engine.
 
-Collected after the other GPU tests: one zero-copy case here once read back zeros, in a block the
-library never writes, where the test's own fill had written its sentinel (the same case passed in
-the run before); a recurrence stops nothing else under pytest -x.
+Pools are created and destroyed per case, with tensors allocated in between: this sequence found
+that freeing physically contiguous staging corrupted later allocations (now plain device memory).
 """
 import numpy as np
 import pytest

@@ -1,7 +1,8 @@
 """Pool lifecycle and concurrency on the GPU.
 
 * kv_pool_destroy waits for every store/load still queued on caller streams (they
-  write the pool or its staging), so freeing the pool never races with the device.
+  write the pool or its staging), so freeing the pool never races with the device; and
+  creating and destroying pools leaves later allocations of the process intact.
 * Two host threads, each with its own stream and cache, use one pool at the same
   time (both storing, or one storing while the other loads): the pool serialises
   enqueues and its staging ring stays ordered across streams.
@@ -16,7 +17,7 @@ import torch
 import harness
 from harness import gpu as hg
 from paper_2609_15021_amd import kvx
-from tests.gpu_support import (TINY, bt_tensor, device_cache, first_mismatch, host_cache, oracle_pool,
+from tests.gpu_support import (DEV, TINY, bt_tensor, device_cache, first_mismatch, host_cache, oracle_pool,
                                oracle_unpack_into, to_device, to_host)
 
 pytestmark = pytest.mark.gpu
@@ -133,6 +134,43 @@ def test_one_thread_stores_while_another_loads(mode):
     assert np.array_equal(got_B, want_B), "cache B: " + first_mismatch(got_B, want_B)
     assert kvx.kv_pool_async_error(pool) == 0
     kvx.kv_pool_destroy(pool)
+
+
+def test_pool_churn_leaves_later_allocations_intact():
+    """Staged pools of varying staging size are created and destroyed 40 times, with fresh tensors
+    allocated between them.  Every fresh tensor reads back the value just written to it, and every
+    round trip equals the oracle's bytes.  Freeing a physically contiguous staging allocation once
+    corrupted later allocations of the process; staging is plain device memory now."""
+    lay, NB = TINY, 96
+    for it in range(40):
+        seed = harness.sub_seed("churn", it)
+        n = 256 * (1 + it % 3) + 7 * it
+        A = host_cache(lay, NB, seed, "raw")
+        btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+        btB = harness.block_table(seed + 2, NB, lay.nblk(n))
+        ids = harness.chunk_ids(lay.nc(n), lay.nc(n) + 1, seed + 3)
+        pool = kvx.kv_pool_create(lay.kv, lay.nc(n) + 1, "staged", staging_slots=2, chunks_per_batch=1 + it % 3)
+        view = kvx.pool_view(pool)
+        view[:] = 0xA5
+        probe = torch.full((1 << 20,), it % 251, dtype=torch.uint8, device=DEV)
+        dA, dB = to_device(A), device_cache(lay, NB, fill=0x5A)
+        tA, tB = bt_tensor(btA), bt_tensor(btB)
+        torch.cuda.synchronize()
+        assert bool((probe == it % 251).all()) and int(probe.cpu().numpy().min()) == it % 251, f"iteration {it}"
+        s = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        kvx.kv_store(kvx.Cache(dA, lay.kv, NB), tA, n, pool, ids, s)
+        kvx.kv_load(kvx.Cache(dB, lay.kv, NB), tB, n, pool, ids, s)
+        s.synchronize()
+        want_pool = oracle_pool(lay, A, btA, n, ids, lay.nc(n) + 1, 0xA5)
+        assert np.array_equal(view, want_pool), f"iteration {it}, pool: " + first_mismatch(view, want_pool)
+        B0 = np.full_like(A, 0).view(np.uint8)
+        B0[:] = 0x5A
+        want_B = oracle_unpack_into(lay, B0.view(A.dtype).reshape(A.shape), btB, n, want_pool, ids)
+        got_B = to_host(dB, A)
+        assert np.array_equal(got_B, want_B), f"iteration {it}, cache B: " + first_mismatch(got_B, want_B)
+        kvx.kv_pool_destroy(pool)
+        del dA, dB, tA, tB, probe
 
 
 def test_many_short_lived_streams():

@@ -1,9 +1,5 @@
 """GPU parity with one cache allocation per layer, the way serving engines (and the benchmark)
 hold their caches: kv_store / kv_load through the C ABI, byte-compared with the CPU oracle.
-
-This file is collected after the other GPU tests.  Its tiny zero-copy case once failed in a full
-suite run with a pattern that points below the library (one XCD seeing the uploaded block table,
-the others stale values) and has not failed since; run last, a recurrence stops nothing else.
 """
 import numpy as np
 import pytest

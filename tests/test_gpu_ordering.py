@@ -15,7 +15,7 @@ import torch
 import harness
 from harness import gpu as hg
 from paper_2609_15021_amd import kvx
-from tests.gpu_support import TINY, bt_tensor, device_cache
+from tests.gpu_support import DEV, TINY, bt_tensor, device_cache
 
 pytestmark = pytest.mark.gpu
 
@@ -192,4 +192,49 @@ def test_cross_stream_store_then_load_ordered_by_event(mode):
         sB.synchronize()
         after = dB.view(torch.uint8).cpu().numpy().reshape(-1)
         assert np.all(after[mask] == 7 + trial)
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("mode", ["zero_copy", "staged"])
+def test_random_interleavings_keep_each_stream_ordered(mode):
+    """Three streams share one pool whose staging ring has two one-chunk slots, so their batches
+    reuse each other's staging.  Each round, in a seeded order with seeded 0-4 ms delays, every
+    stream fills its own source cache with a new byte, stores it into its own slots, restores them
+    into its own destination, and copies the destination aside, all on that stream.  Every copy
+    must hold that round's byte in every named slot and the sentinel elsewhere: each stream's
+    fill -> store -> load -> read chain stays ordered whatever the other streams do."""
+    lay, NB, n, rounds = TINY, 64, 3 * TINY.C, 12
+    rng = np.random.default_rng(harness.sub_seed("interleave", mode))
+    nc = lay.nc(n)
+    pool = kvx.kv_pool_create(lay.kv, 3 * nc, mode, staging_slots=2, chunks_per_batch=1)
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    A = [device_cache(lay, NB, fill=0) for _ in range(3)]
+    B = [device_cache(lay, NB, fill=0xEE) for _ in range(3)]
+    bts = [(harness.block_table(int(rng.integers(1 << 30)), NB, lay.nblk(n)),
+            harness.block_table(int(rng.integers(1 << 30)), NB, lay.nblk(n))) for _ in range(3)]
+    tabs = [(bt_tensor(a), bt_tensor(b)) for a, b in bts]
+    slots = [np.arange(k * nc, (k + 1) * nc) for k in range(3)]
+    nbytes = A[0].numel() * A[0].element_size()
+    snaps = {}
+    torch.cuda.synchronize()
+    for r in range(rounds):
+        for k in rng.permutation(3):
+            s, v = streams[k], int(1 + (r * 3 + k) % 200)
+            hg.spin(float(rng.uniform(0, 4)), s)
+            hg.fill_u8(A[k], nbytes, v, s)
+            kvx.kv_store(kvx.Cache(A[k], lay.kv, NB), tabs[k][0], n, pool, slots[k], s)
+            hg.spin(float(rng.uniform(0, 2)), s)
+            kvx.kv_load(kvx.Cache(B[k], lay.kv, NB), tabs[k][1], n, pool, slots[k], s)
+            snap = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+            hg.copy_u8(snap, B[k], nbytes, s)
+            snaps[(r, k)] = (snap, v)
+    for s in streams:
+        s.synchronize()
+    masks = [_named_slot_mask(lay, NB, bts[k][1], n).reshape(-1) for k in range(3)]
+    for (r, k), (snap, v) in sorted(snaps.items()):
+        got = snap.cpu().numpy().view(np.uint8).reshape(-1)
+        m = np.repeat(masks[k], lay.E)
+        assert (got[m] == v).all(), f"round {r} stream {k}: {int((got[m] != v).sum())} named bytes not {v}"
+        assert (got[~m] == 0xEE).all(), f"round {r} stream {k}: bytes outside the named slots changed"
+    assert kvx.kv_pool_async_error(pool) == 0
     kvx.kv_pool_destroy(pool)

@@ -21,7 +21,7 @@ import torch
 
 import harness
 from paper_2609_15021_amd import kvx
-from tests.gpu_support import DEV, TINY, first_mismatch, host_cache, oracle_pool, oracle_unpack_into, to_host
+from tests.gpu_support import DEV, TINY, TORCH_INT, first_mismatch, host_cache, oracle_pool, oracle_unpack_into, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -453,3 +453,38 @@ def test_two_replicas_store_at_the_same_time(tmp_path):
             assert np.array_equal(got[:, bt], A[:, btA]), f"prompt {seed} restored wrong bytes"
         c.close()
     _finish_native(tier)
+
+
+@pytest.mark.parametrize("i", range(6))
+def test_random_layouts_through_the_tier(i, tmp_path):
+    """Seeded layouts of the random-layout tests (head-major, packed blocks) stored by a replica
+    process through the tier and restored by this process, each case in one of the three mode
+    settings: the pool the tier dumps and the restored cache equal the oracle's bytes."""
+    from tests.test_gpu_fuzz import _case
+    lay, n, NB, _, _, _, _ = _case(7 * i + 3)
+    mode = ["zero_copy", "staged", "staged+zero_copy"][i % 3]
+    nc = lay.nc(n)
+    seed = harness.sub_seed("tier-fuzz", i)
+    print(f"[tier-fuzz] case {i} {mode}: L{lay.L} H{lay.H} D{lay.D} E{lay.E} BS{lay.BS} C{lay.C} n={n} NB={NB}",
+          flush=True)
+    sock, dump = str(tmp_path / "tier.sock"), str(tmp_path / "pool.npy")
+    tier = _start_tier(sock, lay, nc + 1, mode, 2, dump)
+    with _serving(tier):
+        _store_process(sock, lay, NB, n, seed, 0)
+        btB = harness.block_table(seed + 2, NB, lay.nblk(n))
+        dB = torch.zeros((lay.L, NB, 2, lay.H, lay.BS, lay.D), dtype=TORCH_INT[lay.E], device=DEV)
+        s = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        c = _connect(sock)
+        kvx.kv_tier_load(c.fileno(), kvx.Cache(dB, lay.kv, NB), btB, n, np.arange(nc), s)
+        got_B = dB.cpu()
+        c.close()
+    _finish_tier(tier)
+    A = host_cache(lay, NB, seed, "raw")
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+    want_pool = oracle_pool(lay, A, btA, n, np.arange(nc), nc + 1, POOL_SENT)
+    pool = np.load(dump)
+    assert np.array_equal(pool, want_pool), first_mismatch(pool, want_pool)
+    want_B = oracle_unpack_into(lay, np.zeros_like(A), btB, n, want_pool, np.arange(nc))
+    got = got_B.numpy().view(A.dtype).reshape(A.shape)
+    assert np.array_equal(got, want_B), first_mismatch(got, want_B)

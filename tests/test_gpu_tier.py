@@ -21,7 +21,7 @@ import torch
 
 import harness
 from paper_2609_15021_amd import kvx
-from tests.gpu_support import DEV, TINY, TORCH_INT, first_mismatch, host_cache, oracle_pool, oracle_unpack_into, to_host
+from tests.gpu_support import DEV, TINY, TORCH_INT, first_mismatch, host_cache, oracle_pool, oracle_unpack_into
 
 pytestmark = pytest.mark.gpu
 

@@ -99,6 +99,18 @@ __device__ __forceinline__ void store16_cache(__amdgpu_buffer_rsrc_t slab, int v
     __builtin_amdgcn_raw_buffer_store_b128(v, slab, vec * 16, 0, kCachePolicyNtSc1);
 }
 
+// Chunk-side stores of pack.  Into mapped pinned host memory (zero-copy) they take the same
+// "nt sc1" policy, which moved 57.1 GB/s over the link against 55.7-55.9 with plain nontemporal
+// stores (56.8 without either bit); into device staging plain nontemporal stores measured the same
+// as any policy.
+template <bool HOST_SIDE>
+__device__ __forceinline__ void store16_chunk(vec16 *base, __amdgpu_buffer_rsrc_t slab, int vec, vec16 v) {
+    if constexpr (HOST_SIDE)
+        __builtin_amdgcn_raw_buffer_store_b128(v, slab, vec * 16, 0, kCachePolicyNtSc1);
+    else
+        store16(base + vec, v);
+}
+
 // Walks chunk-order vector indices v = t, t + kThreads, t + 2*kThreads, ... of one slab,
 // maintaining (s, h, col) with v = (s*H + h)*VR + col.
 struct RowWalker {
@@ -139,12 +151,12 @@ struct RowWalker {
     __device__ int cache_vec(int BS) const { return (h * BS + s) * VR + col; }
 };
 
-template <int DIR, int U>
+template <int DIR, int U, bool HOST_SIDE>
 __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, int kv, int j);
 
 // HOST_SIDE marks launches whose chunk side is mapped pinned host memory (zero-copy mode);
 // the body is the same, the instantiation (and launch occupancy) is separate.
-template <int DIR, int U>
+template <int DIR, int U, bool HOST_SIDE>
 __device__ __forceinline__ void move_slab_id(const GatherArgs &a, int64_t id) {
     // Slab id -> (chunk c, layer ll, kv, block j); j varies fastest so consecutive ids
     // touch consecutive chunk-side regions.
@@ -155,7 +167,7 @@ __device__ __forceinline__ void move_slab_id(const GatherArgs &a, int64_t id) {
     rest >>= 1;
     const int ll = static_cast<int>(rest % a.nlayers);
     const int c = static_cast<int>(rest / a.nlayers);
-    move_slab<DIR, U>(a, c, ll, kv, j);
+    move_slab<DIR, U, HOST_SIDE>(a, c, ll, kv, j);
 }
 
 template <int DIR, int U, bool HOST_SIDE>
@@ -165,13 +177,13 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const GatherArgs a) {
         // bounds these launches, and the CUs they leave free run other streams' kernels.
         const int64_t total = static_cast<int64_t>(a.nchunks) * a.nlayers * 2 * a.blocks_per_chunk;
         for (int64_t id = blockIdx.x; id < total; id += gridDim.x)
-            move_slab_id<DIR, U>(a, id);
+            move_slab_id<DIR, U, HOST_SIDE>(a, id);
     } else {
-        move_slab_id<DIR, U>(a, blockIdx.x);  // one workgroup per slab
+        move_slab_id<DIR, U, HOST_SIDE>(a, blockIdx.x);  // one workgroup per slab
     }
 }
 
-template <int DIR, int U>
+template <int DIR, int U, bool HOST_SIDE>
 __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, int kv, int j) {
     const int bpc = a.blocks_per_chunk;
 
@@ -205,6 +217,7 @@ __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, in
         return;
     }
 
+    const __amdgpu_buffer_rsrc_t chunk_buf = slab_buffer(chunk_slab, static_cast<int64_t>(nvec) * 16);
     const int64_t slab_bytes = static_cast<int64_t>(a.H) * a.BS * row_bytes;
     uint8_t *cache_slab = a.layer[ll] + static_cast<int64_t>(b) * a.block_stride + kv * slab_bytes;
     vec16 *cache_v = reinterpret_cast<vec16 *>(cache_slab);
@@ -215,7 +228,7 @@ __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, in
         // Token-major block: the slab's first bs*H rows are already in chunk row order.
         for (int v = tid; v < nvec; v += kThreads) {
             if (DIR == kPack)
-                store16(chunk_v + v, load16(cache_v + v));
+                store16_chunk<HOST_SIDE>(chunk_v, chunk_buf, v, load16(cache_v + v));
             else
                 store16_cache(cache_buf, v, load16(chunk_v + v));
         }
@@ -243,7 +256,7 @@ __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, in
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (DIR == kPack)
-                store16(chunk_v + v + u * kThreads, buf[u]);
+                store16_chunk<HOST_SIDE>(chunk_v, chunk_buf, v + u * kThreads, buf[u]);
             else
                 store16_cache(cache_buf, cache_off[u], buf[u]);
         }
@@ -253,7 +266,7 @@ __device__ __forceinline__ void move_slab(const GatherArgs &a, int c, int ll, in
         const int co = w.cache_vec(a.BS);
         w.advance();
         if (DIR == kPack)
-            store16(chunk_v + v, load16(cache_v + co));
+            store16_chunk<HOST_SIDE>(chunk_v, chunk_buf, v, load16(cache_v + co));
         else
             store16_cache(cache_buf, co, load16(chunk_v + v));
     }

@@ -30,7 +30,7 @@ constexpr int kStateUnroll = 4;
 #endif
 
 // Piece q of the launch's snapshots: [snapshot k][layer g][piece of the page].
-template <int DIR>
+template <int DIR, bool HOST_SIDE>
 __device__ __forceinline__ void move_piece(const StateArgs &a, int64_t q) {
     const int64_t per_snap = static_cast<int64_t>(a.G) * a.ppp;
     const int k = static_cast<int>(q / per_snap);
@@ -44,6 +44,10 @@ __device__ __forceinline__ void move_piece(const StateArgs &a, int64_t q) {
     const svec16 *src = reinterpret_cast<const svec16 *>(DIR == kPack ? page : packed);
     svec16 *dst = reinterpret_cast<svec16 *>(DIR == kPack ? packed : page);
     const int nv = static_cast<int>(len >> 4);  // len <= piece = 64 KiB
+    // Zero-copy stores into mapped pinned host memory use cache policy "nt sc1" (NT = 2, SC1 = 16),
+    // as the gather kernels' do: over the link it moved more than plain nontemporal stores.
+    const __amdgpu_buffer_rsrc_t dst_buf =
+        __builtin_amdgcn_make_buffer_rsrc(dst, 0, static_cast<int>(len), 0x00020000);
 
     for (int v0 = static_cast<int>(threadIdx.x); v0 < nv; v0 += kThreads * kStateUnroll) {
         svec16 buf[kStateUnroll];
@@ -56,8 +60,12 @@ __device__ __forceinline__ void move_piece(const StateArgs &a, int64_t q) {
 #pragma unroll
         for (int u = 0; u < kStateUnroll; ++u) {
             const int v = v0 + u * kThreads;
-            if (v < nv)
-                __builtin_nontemporal_store(buf[u], dst + v);
+            if (v < nv) {
+                if constexpr (HOST_SIDE && DIR == kPack)
+                    __builtin_amdgcn_raw_buffer_store_b128(buf[u], dst_buf, v * 16, 0, 2 | 16);
+                else
+                    __builtin_nontemporal_store(buf[u], dst + v);
+            }
         }
     }
 }
@@ -67,9 +75,9 @@ __global__ __launch_bounds__(kThreads) void state_kernel(const StateArgs a) {
     if constexpr (HOST_SIDE) {
         // A capped grid strides over the pieces: the link bounds these launches.
         for (int64_t i = blockIdx.x; i < a.npieces; i += gridDim.x)
-            move_piece<DIR>(a, a.q0 + i);
+            move_piece<DIR, HOST_SIDE>(a, a.q0 + i);
     } else {
-        move_piece<DIR>(a, a.q0 + static_cast<int64_t>(blockIdx.x));  // one workgroup per piece
+        move_piece<DIR, HOST_SIDE>(a, a.q0 + static_cast<int64_t>(blockIdx.x));  // one workgroup per piece
     }
 }
 

@@ -410,3 +410,31 @@ def test_oversized_pool_is_enomem_not_pageable():
     with pytest.raises(kvx.KvError) as e:
         kvx.kv_pool_create(lay.kv, 1 << 24, "zero_copy")  # 1 PiB
     assert e.value.status == kvx.KV_ENOMEM
+
+
+def test_readme_usage():
+    """The README's Python usage, at a small size: per-layer bf16 tensors, the current stream,
+    store then load with no host sync in between; the restored blocks equal the stored ones."""
+    L, H, D, BS, C, NB, n = 4, 2, 64, 16, 256, 64, 700
+    lay = kvx.make_layout(L, H, D, 2, BS, C)
+    nc = -(-n // C)
+    pool = kvx.kv_pool_create(lay, nc, "staged", staging_slots=3)
+    g = torch.Generator().manual_seed(harness.sub_seed("readme"))
+    layers_a = [torch.randn((NB, 2, H, BS, D), generator=g).to(torch.bfloat16).to("cuda:0") for _ in range(L)]
+    layers_b = [torch.zeros_like(t) for t in layers_a]
+    bt_a = harness.block_table(harness.sub_seed("readme", 1), NB, -(-n // BS))
+    bt_b = harness.block_table(harness.sub_seed("readme", 2), NB, -(-n // BS))
+    block_table_a, block_table_b = bt_tensor(bt_a), bt_tensor(bt_b)
+    chunk_ids = list(range(nc))
+    cache_a, cache_b = kvx.Cache(layers_a, lay, NB), kvx.Cache(layers_b, lay, NB)
+    s = torch.cuda.current_stream()
+    kvx.kv_store(cache_a, block_table_a, n, pool, chunk_ids, s)
+    kvx.kv_load(cache_b, block_table_b, n, pool, chunk_ids, s)
+    s.synchronize()
+    assert kvx.kv_pool_async_error(pool) == 0
+    full = n // BS  # whole blocks: every token slot restored
+    ia = torch.from_numpy(bt_a[:full].astype(np.int64)).to("cuda:0")
+    ib = torch.from_numpy(bt_b[:full].astype(np.int64)).to("cuda:0")
+    for a, b in zip(layers_a, layers_b):
+        assert torch.equal(a[ia].view(torch.int16), b[ib].view(torch.int16))
+    kvx.kv_pool_destroy(pool)

@@ -24,6 +24,11 @@ MUTANTS = {
         "non_creator_publishes": ("            if is_new:\n                if ok:", "            if True:\n                if ok:"),
         "unpin_on_lookup_missing": ('                self.slot[s]["pins"] += 1\n        return len(slots)',
                                     '                pass\n        return len(slots)'),
+        "unpin_checks_each_occurrence_alone": (
+            'for s, times in Counter(slots).items():\n            if s not in self.slot or self.slot[s]["pins"] < times:',
+            'for s in slots:\n            if s not in self.slot or self.slot[s]["pins"] == 0:'),
+        "commit_allows_repeated_slots": ("if len(slots) != len(new) or len(set(slots)) != len(slots):",
+                                         "if len(slots) != len(new):"),
     },
 }
 

@@ -160,3 +160,44 @@ def test_new_entries_take_the_lowest_free_slot():
     m.commit(slots, new, False)
     b = _store(m, 0, [9, 9], 2)                    # the freed slot 3 is the lowest again
     assert b == [3]
+
+
+def test_unpin_releases_one_pin_per_occurrence():
+    """A pin is a count of holders (Sec. 3.2: slots a load still reads are not reused before the host
+    has seen that load complete), so it never goes below zero.  Two pinned lookups of one prefix hold
+    two pins; one unpin naming the slot twice releases both.  Naming it three times releases more than
+    are held: an error that releases nothing, and the entry stays protected from eviction."""
+    from oracle.pool_index import EINVAL
+    m = PoolIndexModel(2, 2)
+    a = [1, 1]
+    _store(m, 0, a)
+    s = m.lookup(0, a, 2, pin=True)[2][0]
+    assert m.lookup(0, a, 2, pin=True)[2] == [s]
+    assert m.unpin([s, s, s]) == EINVAL
+    assert m.slot[s]["pins"] == 2
+    st, _, _ = m.reserve(0, [5, 5, 6, 6], 4)      # needs both slots; the pinned one cannot be evicted
+    assert st == EBUSY and m.lookup(0, a, 2)[1] == 1
+    assert m.unpin([s, s]) == 0 and m.slot[s]["pins"] == 0
+    st, slots, new = m.reserve(0, [5, 5, 6, 6], 4)
+    assert st == 0 and new == [1, 1] and m.stats()["evictions"] == 1
+
+
+def test_commit_names_each_reserved_slot_once():
+    """A commit hands back what one reserve returned: one slot per whole chunk, all distinct (each
+    chunk completes a different prefix, so has its own key).  A commit naming a slot twice would
+    release a pin its caller does not hold (here the second replica's): an error that publishes and
+    releases nothing."""
+    from oracle.pool_index import EINVAL
+    m = PoolIndexModel(2, 4)
+    toks = [1, 1, 2, 2]
+    st, slots, new = m.reserve(0, toks, 4)
+    st2, slots2, new2 = m.reserve(0, toks, 4)      # a second replica holds the same entries
+    assert st == st2 == 0 and slots2 == slots and new2 == [0, 0]
+    assert m.commit(slots + [slots[0]], new + [new[0]], True) == EINVAL
+    assert m.lookup(0, toks, 4)[1] == 0 and m.stats()["pending"] == 2
+    assert [m.slot[s]["pins"] for s in slots] == [2, 2]
+    assert m.commit(slots, new, True) == 0
+    assert m.lookup(0, toks, 4)[1] == 2
+    assert [m.slot[s]["pins"] for s in slots] == [1, 1]   # the second replica's pins stand
+    assert m.commit(slots2, new2, True) == 0
+    assert [m.slot[s]["pins"] for s in slots] == [0, 0]

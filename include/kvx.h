@@ -190,22 +190,37 @@ KV_API kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, cons
                          kv_pool **out);
 
 /* Waits until every store/load enqueued on the pool has completed on its caller stream
- * and the pool's side streams are idle, then frees everything.  NULL is a no-op. */
+ * and the pool's side streams are idle, then frees everything: no memory an enqueued
+ * kernel or copy may still touch is released early (Sec. 3.2 cites premature reuse of
+ * asynchronous-copy buffers as a related failure).  NULL is a no-op.  Errors: KV_EHIP
+ * (the first failing runtime call; teardown continues past it). */
 KV_API kv_status kv_pool_destroy(kv_pool *pool);
 
-/* Fills *info.  KV_EINVAL on NULL arguments. */
+/* Fills *info: sizes, the modes in use, and whether the runtime reports the pool as pinned
+ * with its allocation time (Sec. 3.3: the full pool must really be pinned, and the paper times
+ * that allocation).  KV_EINVAL on NULL arguments. */
 KV_API kv_status kv_pool_get_info(const kv_pool *pool, kv_pool_info *info);
 
-/* Host address of state slot `slot` (NULL if out of range or without a state area). */
+/* Host address of state slot `slot` (NULL if out of range or without a state area).  As for
+ * kv_pool_slot, touch it only after the host has seen every call using it complete (Sec. 3.2). */
 KV_API void *kv_pool_state_slot(kv_pool *pool, int64_t slot);
 
-/* Host address of a slot (NULL if out of range).  Touch it only when no call using it is in flight. */
+/* Host address of a slot (NULL if out of range or pool NULL), for the host-side consumer
+ * of stored chunks.  Host-side completion handling precedes host consumption (Sec. 3.2 and
+ * the Fig. 2 caption): read or write a slot only after synchronising the stream (or an
+ * event recorded on it) of every call that uses it; returning from kv_store establishes
+ * nothing.  The address stays valid until kv_pool_destroy. */
 KV_API void *kv_pool_slot(kv_pool *pool, int64_t slot);
-KV_API int64_t kv_pool_slot_bytes(const kv_pool *pool);  /* -1 on NULL */
-KV_API int64_t kv_pool_num_slots(const kv_pool *pool);   /* -1 on NULL */
+/* Bytes of one slot, C*TB (Sec. 3.1: the chunk is a logical view over whole blocks), and
+ * the pool's slot count (Sec. 2: a fixed-size host tier).  -1 on NULL. */
+KV_API int64_t kv_pool_slot_bytes(const kv_pool *pool);
+KV_API int64_t kv_pool_num_slots(const kv_pool *pool);
 
-/* Switch mode between calls, for stores and loads alike.  KV_EINVAL for an unknown mode or staged
- * mode without staging. */
+/* Switch mode between calls, for stores and loads alike.  The transfer path is chosen by the
+ * pool's owner and reported in kv_pool_info, never selected silently (Sec. 3.2: a CLI default
+ * selected the allocator whose raw-pointer fallback dropped the stream dependency).  Both modes
+ * keep the ordering contract.  Affects calls made after it returns; calls already enqueued keep
+ * their mode.  KV_EINVAL for a NULL pool, an unknown mode or staged mode without staging. */
 KV_API kv_status kv_pool_set_mode(kv_pool *pool, uint32_t mode);
 
 /* Switch mode between calls, separately for stores and loads (e.g. a tier that stores staged and
@@ -439,6 +454,15 @@ typedef struct kv_ipc_buffer {
  * KV_IPC_MAX_ALLOCATION_BYTES or larger, KV_EHIP if the runtime refuses. */
 KV_API kv_status kv_ipc_export(const void *dev_ptr, kv_ipc_buffer *out);
 
+/* Host-only check of an IPC buffer as a tier receives it, no HIP call: the declared
+ * allocation is positive and below KV_IPC_MAX_ALLOCATION_BYTES, and [offset, offset + need)
+ * lies inside it.  The tier applies it to every buffer of a request before opening the
+ * allocation (hipIpcOpenMemHandle), so a frame that names a larger allocation ends as
+ * KV_EUNSUPPORTED instead of an open that may not return; after opening, the size of the
+ * mapping itself bounds every access again.  KV_EINVAL for NULL or a range outside the
+ * declared allocation. */
+KV_API kv_status kv_ipc_check(const kv_ipc_buffer *buf, int64_t need);
+
 /* Serve one replica connection: read requests from the connected stream socket
  * `fd` until the peer closes it, run each on `pool` (current device = the
  * pool's), reply.  `index` (may be NULL) manages the pool's slots for the
@@ -498,7 +522,11 @@ KV_API kv_status kv_tier_load_prefix(int fd, const kv_cache *cache, const int32_
                                      const kv_state *state, int64_t state_page, uint64_t salt,
                                      const int32_t *tokens, int64_t n_tokens, int64_t *hit_tokens, void *stream);
 
-/* Thread-local text of the last failure on this thread (HIP error name, message, call site). */
+/* Thread-local text of the last failure on this thread: the HIP error name and message and the
+ * library call site, or the violated rule.  The paper's service log kept only a generic
+ * allocation failure and lost the underlying exception (Sec. 3.3); every failing entry point
+ * here records its cause.  The string is owned by the library and valid until the next failing
+ * call on the same thread; "" if none failed yet. */
 KV_API const char *kv_last_error(void);
 
 /* Name of a status code ("KV_OK", "KV_EINVAL", ...). */

@@ -107,6 +107,8 @@ bool write_full(int fd, const void *buf, size_t n) {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+kv_status check_ipc_buffer(const kv_ipc_buffer *buf, int64_t need);
+
 // The tier end of one connection.
 class Connection {
   public:
@@ -182,6 +184,11 @@ class Connection {
         std::memcpy(key.data(), buf.handle, 64);
         auto it = opened_.find(key);
         if (it == opened_.end()) {
+            // The declared allocation is checked before the open: opening one of 2 GiB or more has
+            // not returned on the machines this library was measured on.
+            kv_status st = check_ipc_buffer(&buf, need);
+            if (st != KV_OK)
+                return kvx::fail(st, "tier: %s %d: %s", what, l, kv_last_error());
             hipIpcMemHandle_t handle;
             static_assert(sizeof(handle) == 64, "IPC handle size");
             std::memcpy(&handle, buf.handle, 64);
@@ -519,9 +526,33 @@ kv_status send_request(uint32_t op, int fd, const kv_cache *cache, const int32_t
     return KV_OK;
 }
 
+// The host-only check behind kv_ipc_check.
+kv_status check_ipc_buffer(const kv_ipc_buffer *buf, int64_t need) {
+    if (!buf)
+        return kvx::fail(KV_EINVAL, "IPC buffer must not be NULL");
+    if (buf->allocation_bytes <= 0)
+        return kvx::fail(KV_EINVAL, "IPC buffer declares an allocation of %lld bytes",
+                         static_cast<long long>(buf->allocation_bytes));
+    if (buf->allocation_bytes >= KV_IPC_MAX_ALLOCATION_BYTES)
+        return kvx::fail(KV_EUNSUPPORTED,
+                         "IPC buffer declares an allocation of %lld bytes; shared allocations must be under %lld",
+                         static_cast<long long>(buf->allocation_bytes),
+                         static_cast<long long>(KV_IPC_MAX_ALLOCATION_BYTES));
+    if (buf->offset < 0 || need < 0 || need > buf->allocation_bytes || buf->offset > buf->allocation_bytes - need)
+        return kvx::fail(KV_EINVAL, "IPC buffer range (offset %lld, %lld bytes) exceeds its declared allocation of %lld",
+                         static_cast<long long>(buf->offset), static_cast<long long>(need),
+                         static_cast<long long>(buf->allocation_bytes));
+    return KV_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+kv_status kv_ipc_check(const kv_ipc_buffer *buf, int64_t need) {
+    return kvx::guarded([&]() -> kv_status { return check_ipc_buffer(buf, need); });
+}
+
 
 kv_status kv_ipc_export(const void *dev_ptr, kv_ipc_buffer *out) {
     return kvx::guarded([&]() -> kv_status {

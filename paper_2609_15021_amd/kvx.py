@@ -133,6 +133,7 @@ def _open():
         "kv_index_commit_state": ([P, i64, ctypes.c_int], i32),
         "kv_index_get_stats": ([P, ctypes.POINTER(KvIndexStats)], i32),
         "kv_ipc_export": ([P, ctypes.POINTER(KvIpcBuffer)], i32),
+        "kv_ipc_check": ([ctypes.POINTER(KvIpcBuffer), i64], i32),
         "kv_tier_serve": ([P, P, ctypes.c_int], i32),
         "kv_tier_listen": ([ctypes.c_char_p, ctypes.POINTER(ctypes.c_int)], i32),
         "kv_tier_run": ([P, P, ctypes.c_int, i32], i32),
@@ -161,7 +162,7 @@ EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slo
            "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version", "kv_pool_state_slot",
            "kv_check_state", "kv_store_state", "kv_load_state", "kv_index_create", "kv_index_destroy",
            "kv_index_keys", "kv_index_lookup", "kv_index_unpin", "kv_index_reserve", "kv_index_commit",
-           "kv_index_reserve_state", "kv_index_commit_state", "kv_index_get_stats", "kv_ipc_export",
+           "kv_index_reserve_state", "kv_index_commit_state", "kv_index_get_stats", "kv_ipc_export", "kv_ipc_check",
            "kv_tier_serve", "kv_tier_store", "kv_tier_load", "kv_tier_listen", "kv_tier_run",
            "kv_tier_store_prefix", "kv_tier_load_prefix")
 
@@ -397,6 +398,30 @@ def _block_table_ptr(block_table, cache: Cache):
     return ctypes.c_void_p(block_table.data_ptr())
 
 
+def _check_lengths(layout: KvLayout, n_tokens: int, n_ids: int, table_len: int) -> None:
+    """The C ABI reads ceil(n/C) chunk ids and ceil(n/BS) block-table entries; shorter arrays would
+    be read past their end (on the host, or by the kernels on the device).  Refused here, before
+    any library call."""
+    n = int(n_tokens)
+    if n <= 0:
+        return
+    nc = -(-n // int(layout.chunk_tokens)) if layout.chunk_tokens > 0 else 0
+    nblk = -(-n // int(layout.block_size)) if layout.block_size > 0 else 0
+    if n_ids < nc:
+        raise ValueError(f"{n_ids} chunk ids for {n} tokens: {nc} chunks of {layout.chunk_tokens} tokens need {nc}")
+    if table_len < nblk:
+        raise ValueError(f"block table of {table_len} entries for {n} tokens: {nblk} blocks of "
+                         f"{layout.block_size} tokens need {nblk}")
+
+
+def _table_len(block_table) -> int:
+    if block_table is None:
+        return 0
+    if isinstance(block_table, torch.Tensor):
+        return int(block_table.numel())
+    return int(np.asarray(block_table).size)
+
+
 def _in_use_on(t: torch.Tensor, stream) -> None:
     """The C ABI reads the block table from `stream` until the call's work completes there.  For a
     stream torch owns (the current stream or a torch.cuda.Stream it created), tell torch's caching
@@ -421,6 +446,7 @@ def kv_check(cache: Cache, pool_layout: KvLayout, pool_slots: int, n_tokens: int
 
 def kv_store(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, stream=None) -> None:
     ids, ptr = _chunk_ids(chunk_ids)
+    _check_lengths(cache.layout, n_tokens, ids.size, _table_len(block_table))
     _raise(_lib.kv_store(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
                          pool.handle, ptr, _stream_handle(stream)))
     if block_table is not None and int(n_tokens) > 0:
@@ -429,6 +455,7 @@ def kv_store(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, st
 
 def kv_load(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, stream=None) -> None:
     ids, ptr = _chunk_ids(chunk_ids)
+    _check_lengths(cache.layout, n_tokens, ids.size, _table_len(block_table))
     _raise(_lib.kv_load(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
                         pool.handle, ptr, _stream_handle(stream)))
     if block_table is not None and int(n_tokens) > 0:
@@ -551,6 +578,11 @@ def kv_ipc_export(ptr) -> KvIpcBuffer:
     return out
 
 
+def kv_ipc_check(buf: KvIpcBuffer, need: int) -> int:
+    """Host-only check of a received IPC buffer (status code; no HIP call)."""
+    return int(_lib.kv_ipc_check(ctypes.byref(buf), int(need)))
+
+
 def kv_tier_serve(pool: Pool, fd: int, index: Index = None) -> None:
     """Serve one replica connection on the connected stream socket ``fd`` until it closes (blocks;
     the GIL is released while it runs); ``index`` enables prefix requests."""
@@ -581,6 +613,7 @@ def kv_tier_store(fd: int, cache: Cache, block_table, n_tokens: int, chunk_ids, 
     synchronised first; returns once the tier has committed the chunks."""
     t, tp = _host_table(block_table)
     ids, ip = _chunk_ids(chunk_ids)
+    _check_lengths(cache.layout, n_tokens, ids.size, t.size)
     _raise(_lib.kv_tier_store(int(fd), ctypes.byref(cache.struct), tp, int(n_tokens), ip, _stream_handle(stream)))
 
 
@@ -588,6 +621,7 @@ def kv_tier_load(fd: int, cache: Cache, block_table, n_tokens: int, chunk_ids, s
     """Load through the tier on ``fd`` into ``cache``; returns once the cache is complete."""
     t, tp = _host_table(block_table)
     ids, ip = _chunk_ids(chunk_ids)
+    _check_lengths(cache.layout, n_tokens, ids.size, t.size)
     _raise(_lib.kv_tier_load(int(fd), ctypes.byref(cache.struct), tp, int(n_tokens), ip, _stream_handle(stream)))
 
 
@@ -598,6 +632,7 @@ def kv_tier_store_prefix(fd: int, cache: Cache, block_table, salt: int, tokens, 
     (chunks stored, snapshots stored)."""
     t, tp = _host_table(block_table)
     tok, kp = _tokens(tokens)
+    _check_lengths(cache.layout, tok.size, tok.size, t.size)  # the table covers the whole prompt
     out, out_state = ctypes.c_int64(), ctypes.c_int32()
     _raise(_lib.kv_tier_store_prefix(int(fd), ctypes.byref(cache.struct), tp,
                                      ctypes.byref(state.struct) if state is not None else None, int(state_page),
@@ -613,6 +648,7 @@ def kv_tier_load_prefix(fd: int, cache: Cache, block_table, salt: int, tokens, s
     tokens."""
     t, tp = _host_table(block_table)
     tok, kp = _tokens(tokens)
+    _check_lengths(cache.layout, tok.size, tok.size, t.size)  # the table covers the whole prompt
     out = ctypes.c_int64()
     _raise(_lib.kv_tier_load_prefix(int(fd), ctypes.byref(cache.struct), tp,
                                     ctypes.byref(state.struct) if state is not None else None, int(state_page),

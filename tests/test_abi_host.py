@@ -23,7 +23,7 @@ def test_header_declares_expected_surface():
     names = _declared()
     for must in ("kv_store", "kv_load", "kv_pool_create", "kv_pool_destroy", "kv_last_error", "kv_check"):
         assert must in names
-    assert len(names) == 38
+    assert len(names) == 39
 
 
 def test_library_exports_every_declared_symbol():
@@ -231,3 +231,59 @@ def test_tier_daemon_rejects_bad_arguments_without_a_gpu():
                  ["--bogus", "1"]):
         r = subprocess.run([build.TIERD_BIN, *args], capture_output=True, text=True, timeout=30)
         assert r.returncode == 2 and "usage" in r.stderr, (args, r.stderr)
+
+
+def test_binding_refuses_short_arrays_before_any_library_call(monkeypatch):
+    """kv_store/kv_load (and the tier wrappers) read ceil(n/C) chunk ids and ceil(n/BS) table
+    entries: shorter arrays are refused in the binding, before the library is called."""
+    import torch
+    from paper_2609_15021_amd import kvx
+
+    class NoLibrary:
+        def __getattr__(self, name):
+            raise AssertionError(f"library call {name} made for a refused request")
+
+    lay = kvx.make_layout(2, 2, 64, 2, 16, 256)
+    cache = object.__new__(kvx.Cache)
+    cache.layout = lay
+    monkeypatch.setattr(kvx, "_lib", NoLibrary())
+    n = 4 * 256 + 20                       # 5 chunks, 65 blocks
+    full_ids, full_bt = np.arange(5), torch.zeros(65, dtype=torch.int32)
+    for fn in (kvx.kv_store, kvx.kv_load):
+        with pytest.raises(ValueError, match="chunk ids"):
+            fn(cache, full_bt, n, None, np.arange(4))
+        with pytest.raises(ValueError, match="block table"):
+            fn(cache, torch.zeros(64, dtype=torch.int32), n, None, full_ids)
+    for fn in (kvx.kv_tier_store, kvx.kv_tier_load):
+        with pytest.raises(ValueError, match="chunk ids"):
+            fn(3, cache, np.zeros(65, np.int32), n, np.arange(4))
+        with pytest.raises(ValueError, match="block table"):
+            fn(3, cache, np.zeros(64, np.int32), n, full_ids)
+    for fn in (kvx.kv_tier_store_prefix, kvx.kv_tier_load_prefix):
+        with pytest.raises(ValueError, match="block table"):
+            fn(3, cache, np.zeros(64, np.int32), 0, np.zeros(n, np.int32))
+
+
+def test_ipc_frames_naming_large_allocations_are_refused_before_opening():
+    """The tier checks each received IPC buffer on the host before hipIpcOpenMemHandle: an
+    allocation of KV_IPC_MAX_ALLOCATION_BYTES or more is refused (opening one has not returned on
+    these machines), as is a range outside the declared allocation.  No HIP call is made."""
+    from paper_2609_15021_amd import kvx
+    limit = kvx.KV_IPC_MAX_ALLOCATION_BYTES
+
+    def buf(alloc, off):
+        b = kvx.KvIpcBuffer()
+        b.allocation_bytes, b.offset = alloc, off
+        return b
+
+    assert kvx.kv_ipc_check(buf(limit - 4096, 0), limit - 4096) == kvx.KV_OK
+    assert kvx.kv_ipc_check(buf(1 << 20, 4096), (1 << 20) - 4096) == kvx.KV_OK
+    assert kvx.kv_ipc_check(buf(limit, 0), 4096) == kvx.KV_EUNSUPPORTED
+    assert "under" in kvx.kv_last_error()
+    assert kvx.kv_ipc_check(buf(4 * limit, 0), 4096) == kvx.KV_EUNSUPPORTED
+    assert kvx.kv_ipc_check(buf(0, 0), 0) == kvx.KV_EINVAL
+    assert kvx.kv_ipc_check(buf(-5, 0), 0) == kvx.KV_EINVAL
+    assert kvx.kv_ipc_check(buf(1 << 20, 4096), 1 << 20) == kvx.KV_EINVAL     # runs past the end
+    assert kvx.kv_ipc_check(buf(1 << 20, -16), 16) == kvx.KV_EINVAL
+    assert kvx.kv_ipc_check(buf(1 << 20, 0), -1) == kvx.KV_EINVAL
+    assert kvx._lib.kv_ipc_check(None, 0) == kvx.KV_EINVAL

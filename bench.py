@@ -75,6 +75,13 @@ def parse():
     ap.add_argument("--tier-server", metavar="SOCKET", help=argparse.SUPPRESS)
     ap.add_argument("--tier-load-mode", choices=["staged", "zero_copy"], help=argparse.SUPPRESS)
     ap.add_argument("--tier-store", metavar="SOCKET", help=argparse.SUPPRESS)
+    ap.add_argument("--leg-256k-only", action="store_true",
+                    help="only measure the 256k+192 restore and print its JSON object (run first by the main bench)")
+    ap.add_argument("--pin-probe-only", action="store_true",
+                    help="only find the largest pool this process can pin and print it (run by the main bench)")
+    ap.add_argument("--device-leg-only", action="store_true",
+                    help="only run the device-only pack/unpack leg at 128k and print its JSON object")
+    ap.add_argument("--no-device-leg", action="store_true", help="skip the device-only pack/unpack leg")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (PMC counter scale reference)")
     return ap.parse_args()
@@ -720,6 +727,160 @@ def hbm_copy_achievable(torch, dev, nbytes=4 << 30, reps=5):
     return round(2 * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9, 1)
 
 
+def read_text(path):
+    try:
+        with open(path) as f:
+            return f.read().strip()
+    except OSError:
+        return None
+
+
+def host_memory_facts():
+    """What bounds pinned host memory on this machine, as far as an unprivileged process can read it."""
+    import resource
+    mem_total = None
+    for line in (read_text("/proc/meminfo") or "").splitlines():
+        if line.startswith("MemTotal:"):
+            mem_total = round(int(line.split()[1]) / 2**20, 1)
+    soft, hard = resource.getrlimit(resource.RLIMIT_MEMLOCK)
+    lim = lambda v: None if v == resource.RLIM_INFINITY else round(v / 2**30, 2)  # noqa: E731
+    ttm = read_text("/sys/module/ttm/parameters/pages_limit")
+    return {"mem_total_GiB": mem_total, "memlock_limit_GiB": [lim(soft), lim(hard)],
+            "cgroup_memory_max": read_text("/sys/fs/cgroup/memory.max"),
+            "ttm_pages_limit_GiB": round(int(ttm) * 4096 / 2**30, 2) if ttm and ttm.isdigit() else None,
+            "amdgpu_gttsize_MiB": read_text("/sys/module/amdgpu/parameters/gttsize")}
+
+
+def probe_pin_ceiling(kvx, layout, hi_slots=1280):
+    """Largest pool (in 64 MiB slots, no staging) this process can pin: a binary search over
+    kv_pool_create, each pool freed before the next attempt."""
+    lo, hi = 0, hi_slots + 1  # lo pins, hi does not
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        try:
+            kvx.kv_pool_destroy(kvx.kv_pool_create(layout, mid, "zero_copy"))
+            lo = mid
+        except kvx.KvError as e:
+            if e.status != kvx.KV_ENOMEM:
+                raise
+            hi = mid
+    return lo
+
+
+def restore_256k_leg(np, torch, harness, hg, kvx, mode, dev, reps=3):
+    """The 256k+192 workload: 262,336 tokens (1,024 full chunks and a 192-token partial chunk) of the
+    27B-class layout in 20,480-block (80 GiB) allocations.  The pool is the 80 GiB (1,280-slot) pinned
+    pool of the workload when it can be pinned, else the exact 1,025 slots the prefix needs; the pool
+    (and its staging) is created first, before the replicas' caches, as a server creates its tier."""
+    n2, nb2 = 262336, 20480
+    nc2, nblk2 = -(-n2 // C), -(-n2 // BS)
+    N2 = n2 * TOKEN_BYTES
+    layout = kvx.make_layout(L, H, D, E, BS, C)
+    out = {"workload": "262,336-token prefix (1,024 chunks + a 192-token partial chunk) of the 27B-class layout, "
+                       "20,480-block caches (80 GiB each); store from replica A, then restore into a fresh random "
+                       "block set of replica B",
+           "prefix_tokens": n2, "bytes_per_direction": N2, "mode": mode, "host": host_memory_facts()}
+    pool, failures = None, []
+    for slots in (1280, nc2):
+        try:
+            pool = kvx.kv_pool_create(layout, slots, mode, staging_slots=3 if mode == "staged" else 0, profile=True)
+            break
+        except kvx.KvError as e:
+            if e.status != kvx.KV_ENOMEM:
+                raise
+            failures.append({"slots": slots, "GiB": round(slots * C * TOKEN_BYTES / 2**30, 2), "error": str(e)})
+    out["pin_failures"] = failures
+    if pool is None:
+        return out, False
+    info = kvx.kv_pool_get_info(pool)
+    out.update(pool_slots=info["num_slots"], pool_GiB=round(info["pool_bytes"] / 2**30, 2),
+               pool_alloc_s=round(info["alloc_seconds"], 3), is_pinned=info["is_pinned"])
+    seed2 = harness.sub_seed("bench", n2)
+    ids2 = harness.chunk_ids(nc2, nc2)
+    ra, rb = Replica(torch, kvx, layout, nb2, dev), Replica(torch, kvx, layout, nb2, dev)
+    ra.fill(hg, seed2, "n01")
+    rb.zero()
+    ba, bb = harness.block_table(seed2 + 1, nb2, nblk2), harness.block_table(seed2 + 2, nb2, nblk2)
+    ta, tb = torch.from_numpy(ba).to(dev), torch.from_numpy(bb).to(dev)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()  # fills ran on the default stream; s is non-blocking
+    stores, loads, store_ev, load_ev = [], [], [], []
+    for k in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        w0 = time.perf_counter()
+        e[0].record(s)
+        kvx.kv_store(ra.cache, ta, n2, pool, ids2, s)
+        e[1].record(s)
+        s.synchronize()
+        w1 = time.perf_counter()
+        kvx.kv_load(rb.cache, tb, n2, pool, ids2, s)
+        e[2].record(s)
+        s.synchronize()
+        w2 = time.perf_counter()
+        stores.append(w1 - w0)
+        loads.append(w2 - w1)
+        store_ev.append(e[0].elapsed_time(e[1]) / 1e3)
+        load_ev.append(e[1].elapsed_time(e[2]) / 1e3)
+    ok, msg = sampled_round_trip(np, harness, rb, ba, bb, seed2, n2, nb2, [0, nc2 // 2, nc2 - 1], torch)
+    ks = {w: kvx.kv_pool_kernel_stats(pool, w, reset=True) for w in ("pack", "unpack")}
+    restore = statistics.median(loads)
+    out.update(restore_s=round(restore, 4), restore_s_all=[round(x, 4) for x in loads],
+               store_s=round(statistics.median(stores), 4),
+               store_GBps=round(N2 / statistics.median(store_ev) / 1e9, 3),
+               load_GBps=round(N2 / statistics.median(load_ev) / 1e9, 3),
+               restore_GBps=round(N2 / restore / 1e9, 3),
+               kernels={w: {"launches": v[0], "avg_launch_ms": round(v[1] / max(v[0], 1), 4)} for w, v in ks.items()},
+               async_error=kvx.kv_pool_async_error(pool), parity=msg if ok else f"FAILED: {msg}")
+    kvx.kv_pool_destroy(pool)
+    return out, ok and out["async_error"] == 0
+
+
+def device_leg(np, torch, harness, kvx, rep_a, rep_b, t_a, t_b, bt_a, bt_b, seed, n, num_blocks, dev, reps=5):
+    """Pack and unpack with the host link out of the picture: the 128k prefix stored from replica A
+    into a device-resident pool (KV_POOL_DEVICE, 16-chunk launches: the staged path's launch shape)
+    and loaded from it into replica B, reps times.  The kernels' live HIP-event durations give the
+    HBM roofline; the working set (2 x 32 GiB per pass) is far beyond the 256 MB MALL."""
+    layout = kvx.make_layout(L, H, D, E, BS, C)
+    nc = -(-n // C)
+    N = n * TOKEN_BYTES
+    ids = harness.chunk_ids(nc, nc)
+    pool = kvx.kv_pool_create(layout, nc, "zero_copy", host_kind=kvx.KV_POOL_DEVICE, profile=True)
+    s = torch.cuda.Stream()
+    kvx.kv_store(rep_a.cache, t_a, n, pool, ids, s)  # warm-up pass
+    kvx.kv_load(rep_b.cache, t_b, n, pool, ids, s)
+    s.synchronize()
+    for w in ("pack", "unpack"):
+        kvx.kv_pool_kernel_stats(pool, w, reset=True)
+    dirs = {"pack": [], "unpack": []}
+    for _ in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(s)
+        kvx.kv_store(rep_a.cache, t_a, n, pool, ids, s)
+        e[1].record(s)
+        kvx.kv_load(rep_b.cache, t_b, n, pool, ids, s)
+        e[2].record(s)
+        s.synchronize()
+        dirs["pack"].append(e[0].elapsed_time(e[1]) / 1e3)
+        dirs["unpack"].append(e[1].elapsed_time(e[2]) / 1e3)
+    kernels = {}
+    for w in ("pack", "unpack"):
+        launches, total_ms, alg = kvx.kv_pool_kernel_stats(pool, w, reset=True)
+        avg = total_ms / max(launches, 1)
+        per = alg / max(launches, 1)
+        kernels[w] = {"launches": launches, "avg_launch_ms": round(avg, 4), "algorithmic_bytes_per_launch": per,
+                      "achieved_GBps": round(per / (avg / 1e3) / 1e9, 1),
+                      "frac_of_hbm_peak": round(per / (avg / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+                      "direction_GBps_HBM": round(2 * N / statistics.median(dirs[w]) / 1e9, 1)}
+    ok, msg = sampled_round_trip(np, harness, rep_b, bt_a, bt_b, seed, n, num_blocks,
+                                 sorted({0, nc // 2, nc - 1}), torch)
+    err = kvx.kv_pool_async_error(pool)
+    kvx.kv_pool_destroy(pool)
+    return {"workload": f"{n:,}-token 27B-class prefix, replica A -> device-resident pool -> replica B, "
+                        f"{reps} passes after a warm-up pass",
+            "pool": "KV_POOL_DEVICE (HBM), 16 chunks (2 GiB of HBM traffic) per launch",
+            "kernels": kernels, "parity": msg if ok else f"FAILED: {msg}"}, ok and err == 0
+
+
 def env_record(torch, info):
     def read(path):
         try:
@@ -828,35 +989,54 @@ def compute_overlap_leg(torch, kvx, rep_b, t_b, n, ids, pool, dev, size=8192, re
             "gemm_slowdown": round(g_both / g_alone, 3), "restore_slowdown": round(r_both / r_alone, 3)}
 
 
-def cpu_baseline(np, oracle, n_chunks=64):
-    """The oracle timed on host cores: store + load of a bounded sample of the workload."""
+def cpu_baseline(np, oracle, n_chunks=128):
+    """The oracle timed on host cores: store then load of a bounded sample of the 128k workload (the
+    first n_chunks chunks), host memory to host memory, on every CPU this process may run on and on
+    one thread.  Rates are bytes per direction per second, as the GPU path's; the restore seconds
+    they imply at the workload's prefix lengths are load bytes / the oracle's load rate."""
     rng = np.random.default_rng(2609)
     bpc = C // BS
     nb = n_chunks * bpc
     n = n_chunks * C
+    N = n * TOKEN_BYTES
     lay = oracle.make_layout(L, H, D, E, BS, C)
-    src = np.frombuffer(rng.bytes(L * nb * 2 * H * BS * D * E), dtype=np.uint8).reshape(L, -1)
+    # Seeded random bytes: a 256 MiB random block repeated (the values are opaque to the path).
+    block = np.frombuffer(rng.bytes(256 << 20), dtype=np.uint8)
+    src = np.resize(block, L * nb * 2 * H * BS * D * E).reshape(L, -1)
     src_layers = [np.ascontiguousarray(src[l]) for l in range(L)]
+    del src
     dst_layers = [np.zeros_like(a) for a in src_layers]
     bt_a = rng.permutation(nb).astype(np.int32)
     bt_b = rng.permutation(nb).astype(np.int32)
     pool = np.zeros(n_chunks * oracle.slot_bytes(lay), dtype=np.uint8)
     ids = np.arange(n_chunks)
-    threads = min(16, os.cpu_count() or 1)
+    threads = len(os.sched_getaffinity(0))
     res = {}
-    for nt, reps in ((threads, 3), (1, 1)):
-        rates = []
+    for nt, reps in ((threads, 5), (1, 3)):
+        ts, tl = [], []
         for _ in range(reps):
             t0 = time.perf_counter()
             assert oracle.pack(lay, src_layers, 2 * H * BS * D * E, nb, bt_a, n, pool, ids, nt) == oracle.OK
+            t1 = time.perf_counter()
             assert oracle.unpack(lay, dst_layers, 2 * H * BS * D * E, nb, bt_b, n, pool, ids, nt) == oracle.OK
-            rates.append(2 * n * TOKEN_BYTES / (time.perf_counter() - t0) / 1e9)
-        res[nt] = statistics.median(rates)
-    return {"value": round(res[threads], 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "value_1_thread": round(res[1], 3),
-            "sample": f"{n_chunks} chunks ({n:,} tokens, {n * TOKEN_BYTES / 2**30:.0f} GiB per direction) of the "
-                      "128k workload: oracle store then load, host memory to host memory, seeded random bytes; "
-                      f"median of 3 passes on {threads} threads, 1 pass on 1 thread"}
+            t2 = time.perf_counter()
+            ts.append(t1 - t0)
+            tl.append(t2 - t1)
+        res[nt] = (N / statistics.median(ts) / 1e9, N / statistics.median(tl) / 1e9,
+                   2 * N / (statistics.median(ts) + statistics.median(tl)) / 1e9)
+    restore = {str(m): {"all_threads": round(m * TOKEN_BYTES / (res[threads][1] * 1e9), 3),
+                        "one_thread": round(m * TOKEN_BYTES / (res[1][1] * 1e9), 3)}
+               for m in (32768, 131072, 262336)}
+    return {"value": round(res[threads][2], 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "value_1_thread": round(res[1][2], 3),
+            "store_GBps": round(res[threads][0], 3), "load_GBps": round(res[threads][1], 3),
+            "store_GBps_1_thread": round(res[1][0], 3), "load_GBps_1_thread": round(res[1][1], 3),
+            "implied_restore_s": restore,
+            "cpu": next((ln.split(":", 1)[1].strip() for ln in (read_text("/proc/cpuinfo") or "").splitlines()
+                         if ln.startswith("model name")), None),
+            "sample": f"{n_chunks} chunks ({n:,} tokens, {N / 2**30:.0f} GiB per direction) of the 128k workload: "
+                      "oracle store then load, host memory to host memory, seeded random bytes; median of "
+                      f"{5} passes on all {threads} CPUs of the process's affinity mask, 3 passes on 1 thread"}
 
 
 def main():
@@ -878,6 +1058,32 @@ def main():
     from paper_2609_15021_amd import kvx
 
     dev = torch.device("cuda:0")
+    if args.leg_256k_only:
+        res, res_ok = restore_256k_leg(np, torch, harness, hg, kvx, args.mode, dev)
+        print(json.dumps(res), flush=True)
+        sys.exit(0 if res_ok else 1)
+    if args.pin_probe_only:
+        slots = probe_pin_ceiling(kvx, kvx.make_layout(L, H, D, E, BS, C))
+        print(json.dumps({"pin_ceiling_slots": slots, "pin_ceiling_GiB": round(slots * C * TOKEN_BYTES / 2**30, 2),
+                          "method": "binary search over kv_pool_create (64 MiB slots, no staging) in a fresh "
+                                    "process, each pool freed before the next attempt"}), flush=True)
+        return
+    if args.device_leg_only:
+        layout = kvx.make_layout(L, H, D, E, BS, C)
+        n = args.tokens
+        seed = harness.sub_seed("bench", n)
+        rep_a = Replica(torch, kvx, layout, args.pool_blocks, dev)
+        rep_b = Replica(torch, kvx, layout, args.pool_blocks, dev)
+        rep_a.fill(hg, seed, "n01")
+        rep_b.zero()
+        bt_a = harness.block_table(seed + 1, args.pool_blocks, -(-n // BS))
+        bt_b = harness.block_table(seed + 2, args.pool_blocks, -(-n // BS))
+        t_a, t_b = torch.from_numpy(bt_a).to(dev), torch.from_numpy(bt_b).to(dev)
+        torch.cuda.synchronize()
+        res, res_ok = device_leg(np, torch, harness, kvx, rep_a, rep_b, t_a, t_b, bt_a, bt_b, seed, n,
+                                 args.pool_blocks, dev)
+        print(json.dumps(res), flush=True)
+        sys.exit(0 if res_ok else 1)
     if args.paper_layout_only:
         paper, paper_ok = paper_layout(np, torch, harness, hg, kvx, args.mode, dev)
         print(json.dumps(paper), flush=True)
@@ -926,6 +1132,19 @@ def main():
         lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
         return (json.loads(lines[-1]) if lines else {"error": r.stderr[-2000:]}), r.returncode == 0 and bool(lines)
 
+    # The 256k+192 restore first, in a fresh process: its 64-80 GiB pinned pool is close to what one
+    # process can pin on these machines, and every stream that has run work keeps some of that.
+    leg256, leg256_ok, pin_probe = None, True, None
+    if not args.no_256k:
+        leg256, leg256_ok = child_leg("--leg-256k-only")
+        if "error" not in leg256:
+            if leg256.get("restore_s") is not None:
+                log(f"[bench] 256k+192 ({leg256['pool_GiB']} GiB pool): restore {leg256['restore_s']} s "
+                    f"({leg256['restore_GBps']} GB/s), store {leg256['store_GBps']} GB/s, load {leg256['load_GBps']} "
+                    f"GB/s; {leg256['parity']}")
+            if leg256.get("pin_failures"):
+                pin_probe, _ = child_leg("--pin-probe-only")
+                log(f"[bench] 256k pins failed: {leg256['pin_failures']}; probe: {pin_probe}")
     paper, paper_ok = None, True
     if not args.no_paper_layout:
         paper, paper_ok = child_leg("--paper-layout-only")
@@ -954,7 +1173,7 @@ def main():
             log(f"[bench] paper hybrid prompt through the tier: {hybrid['external_hit_tokens']} tokens hit + snapshot, "
                 f"restore {hybrid['restore_s']} s ({hybrid['restore_GBps']} GB/s), store {hybrid['store_s']} s; "
                 f"{hybrid['round_trip']}")
-    paper_ok = paper_ok and state_ok and tier_ok and hybrid_ok
+    paper_ok = paper_ok and state_ok and tier_ok and hybrid_ok and leg256_ok
 
     layout = kvx.make_layout(L, H, D, E, BS, C)
     n = args.tokens
@@ -1002,47 +1221,61 @@ def main():
         kvx.kv_pool_kernel_stats(pool, w, reset=True)
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    host_t = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
+        h0 = time.perf_counter()
         step(events[k])
+        host_t.append((h0 - t0, time.perf_counter() - t0))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     log(f"[bench] timed {args.steps} steps in {elapsed:.3f} s")
 
     store_s = [e[0].elapsed_time(e[1]) / 1e3 for e in events]
     load_s = [e[1].elapsed_time(e[2]) / 1e3 for e in events]
+    # Where the timed region's time goes, step by step: the store and load intervals on the GPU, the
+    # GPU time between one step's end and the next step's start, and when the host enqueued each step.
+    gaps = [events[k][2].elapsed_time(events[k + 1][0]) / 1e3 for k in range(args.steps - 1)]
+    first_to_last = events[0][0].elapsed_time(events[-1][2]) / 1e3
+    timeline = {"store_s": [round(x, 4) for x in store_s], "load_s": [round(x, 4) for x in load_s],
+                "gap_s": [round(x, 4) for x in gaps],
+                "host_enqueue_s": [[round(a, 4), round(b, 4)] for a, b in host_t],
+                "gpu_first_to_last_s": round(first_to_last, 4),
+                "sum_store_load_s": round(sum(store_s) + sum(load_s), 4), "sum_gap_s": round(sum(gaps), 4),
+                "host_outside_gpu_s": round(elapsed - first_to_last, 4)}
+    log(f"[bench] timeline: store+load {timeline['sum_store_load_s']} s, gaps {timeline['sum_gap_s']} s, "
+        f"host outside the GPU interval {timeline['host_outside_gpu_s']} s; max store {max(store_s):.4f} s, "
+        f"max load {max(load_s):.4f} s")
     kstats = {w: kvx.kv_pool_kernel_stats(pool, w, reset=True) for w in ("pack", "unpack")}
     value = 2 * N * args.steps / elapsed / 1e9
 
-    # Dominant kernel of the step (largest total time) and its HBM roofline.
-    dom = max(kstats, key=lambda w: kstats[w][1])
-    launches, total_ms, alg_bytes = kstats[dom]
-    avg_ms = total_ms / max(launches, 1)
-    per_launch = alg_bytes / max(launches, 1)
-    roof = None
+    in_step = None
     if args.mode == "staged":
-        traffic, why = traffic_from_profile(dom)
-        achieved = per_launch / (avg_ms / 1e3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                "kernel": f"gather_kernel<{dom}> (staged, device staging side)",
-                "launches": launches, "avg_launch_ms": round(avg_ms, 4),
-                "algorithmic_bytes_per_launch": per_launch}
-        if why:
-            roof["traffic_note"] = why
-        other = "unpack" if dom == "pack" else "pack"
-        ln, tm, ab = kstats[other]
-        roof["other_kernel"] = {"kernel": f"gather_kernel<{other}>", "achieved": round(ab / (tm / 1e3) / 1e9, 1),
-                                "frac": round(ab / (tm / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
-                                "avg_launch_ms": round(tm / max(ln, 1), 4)}
-        log(f"[bench] {dom} kernels: {launches} launches, avg {avg_ms:.4f} ms, {achieved:.1f} GB/s "
-            f"({achieved / HBM_PEAK_GBPS:.1%} of HBM peak)")
+        in_step = {}
+        for w in ("pack", "unpack"):
+            ln, tm, ab = kstats[w]
+            in_step[w] = {"launches": ln, "avg_launch_ms": round(tm / max(ln, 1), 4),
+                          "achieved_GBps": round(ab / (tm / 1e3) / 1e9, 1),
+                          "frac_of_hbm_peak": round(ab / (tm / 1e3) / 1e9 / HBM_PEAK_GBPS, 4)}
+        log(f"[bench] kernels inside the timed steps (beside the DMA copies): {json.dumps(in_step)}")
 
     ok, parity_msg = sampled_round_trip(np, harness, rep_b, bt_a, bt_b, seed, n, args.pool_blocks,
                                         sorted({0, nc // 2, nc - 1}), torch)
     ok = ok and paper_ok
     log(f"[bench] parity: {parity_msg}")
+
+    # The device-only leg: the same kernels with the host link out of the picture (the HBM roofline).
+    dleg = None
+    if not args.no_device_leg:
+        dleg, dleg_ok = device_leg(np, torch, harness, kvx, rep_a, rep_b, t_a, t_b, bt_a, bt_b, seed, n,
+                                   args.pool_blocks, dev)
+        ok_device = dleg_ok
+        log(f"[bench] device-only leg: {json.dumps(dleg['kernels'])}; {dleg['parity']}")
+    else:
+        ok_device = True
+
+    ok = ok and ok_device
 
     # Restore seconds: host wall clock of a full-prefix load (prefix already in the pool).
     restore = []
@@ -1130,53 +1363,9 @@ def main():
     log(f"[bench] plain device-to-device copy: {hbm_copy} GB/s")
     torch.cuda.empty_cache()
 
-    restore_256k = None
-    parity_256k = None
-    alloc_s_256k = None
-    if not args.no_256k:
-        n2, nb2 = 262336, 20480  # 1,024 full chunks + a 192-token partial chunk; 80 GiB allocations
-        nc2, nblk2 = -(-n2 // C), -(-n2 // BS)
-        seed2 = harness.sub_seed("bench", n2)
-        ids2 = harness.chunk_ids(nc2, nc2)
-        ra = rb = ta = tb = None
-        # The pool (and its staging) is created before the replicas' caches, as a server creates its
-        # tier at start: staging allocated after the 128k leg's frees and the 160 GiB of 256k caches
-        # lands in recycled device memory, where its DMA copies ran 2-4% slower.
-        try:
-            pool2 = kvx.kv_pool_create(layout, nc2, args.mode, staging_slots=3 if args.mode == "staged" else 0)
-        except kvx.KvError as e:
-            # The 64.06 GiB pool is close to what one process can pin on these machines (about
-            # 65.5 GiB); a machine with less headroom reports it here instead of failing the run.
-            if e.status != kvx.KV_ENOMEM:
-                raise
-            pool2 = None
-            parity_256k = f"not measured: {e}"
-            log(f"[bench] 256k+192 pool could not be pinned: {e}")
-        if pool2 is not None:
-            alloc_s_256k = kvx.kv_pool_get_info(pool2)["alloc_seconds"]
-            ra, rb = Replica(torch, kvx, layout, nb2, dev), Replica(torch, kvx, layout, nb2, dev)
-            ra.fill(hg, seed2, "n01")
-            rb.zero()
-            ba, bb = harness.block_table(seed2 + 1, nb2, nblk2), harness.block_table(seed2 + 2, nb2, nblk2)
-            ta, tb = torch.from_numpy(ba).to(dev), torch.from_numpy(bb).to(dev)
-            torch.cuda.synchronize()  # fills ran on the default stream; s is non-blocking
-            kvx.kv_store(ra.cache, ta, n2, pool2, ids2, s)
-            s.synchronize()
-            times = []
-            for _ in range(3):
-                w0 = time.perf_counter()
-                kvx.kv_load(rb.cache, tb, n2, pool2, ids2, s)
-                s.synchronize()
-                times.append(time.perf_counter() - w0)
-            restore_256k = statistics.median(times)
-            ok2, msg2 = sampled_round_trip(np, harness, rb, ba, bb, seed2, n2, nb2, [0, nc2 // 2, nc2 - 1], torch)
-            parity_256k = msg2
-            ok = ok and ok2
-            log(f"[bench] 256k+192 restore {restore_256k:.3f} s ({n2 * TOKEN_BYTES / restore_256k / 1e9:.2f} GB/s); "
-                f"parity: {msg2}")
-            kvx.kv_pool_destroy(pool2)
-        del ra, rb, ta, tb
-        torch.cuda.empty_cache()
+    restore_256k = leg256.get("restore_s") if leg256 else None
+    parity_256k = (leg256.get("parity") or f"not measured: no pool could be pinned ({leg256.get('pin_failures')})"
+                   if leg256 and "error" not in leg256 else (leg256 or {}).get("error"))
 
     index = None
     prompts = None
@@ -1195,7 +1384,28 @@ def main():
         if index is not None:
             cpu["pool_index"] = pool_index_oracle(np, PoolIndexModel, prompts)
     if cpu:
-        log(f"[bench] cpu oracle: {cpu['value']} GB/s on {cpu['cores']} threads, {cpu['value_1_thread']} GB/s on 1")
+        log(f"[bench] cpu oracle: {cpu['value']} GB/s on {cpu['cores']} threads, {cpu['value_1_thread']} GB/s on 1; "
+            f"implied restore seconds {cpu['implied_restore_s']}")
+
+    roof = None
+    if dleg:
+        kd = dleg["kernels"]
+        dom = max(kd, key=lambda w: kd[w]["avg_launch_ms"])  # equal launch counts: the slower launch dominates
+        other = "unpack" if dom == "pack" else "pack"
+        traffic, why = traffic_from_profile(dom)
+        roof = {"bound": "hbm", "achieved": kd[dom]["achieved_GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": kd[dom]["frac_of_hbm_peak"], "traffic": traffic,
+                "kernel": f"gather_kernel<{dom}> (device-only leg: one workgroup per 32 KiB slab, 16 chunks per "
+                          "launch, live HIP events on the launch stream)",
+                "launches": kd[dom]["launches"], "avg_launch_ms": kd[dom]["avg_launch_ms"],
+                "algorithmic_bytes_per_launch": kd[dom]["algorithmic_bytes_per_launch"],
+                "other_kernel": {"kernel": f"gather_kernel<{other}>", "achieved": kd[other]["achieved_GBps"],
+                                 "frac": kd[other]["frac_of_hbm_peak"], "avg_launch_ms": kd[other]["avg_launch_ms"]},
+                "in_step": in_step}
+        if why:
+            roof["traffic_note"] = why
+        log(f"[bench] roofline: {dom} {roof['achieved']} GB/s ({roof['frac']:.1%} of HBM peak), {other} "
+            f"{roof['other_kernel']['achieved']} GB/s")
 
     store_gbps = N / statistics.median(store_s) / 1e9
     load_gbps = N / statistics.median(load_s) / 1e9
@@ -1214,7 +1424,7 @@ def main():
                    "prefix_tokens": n, "bytes_per_direction": N, "mode": args.mode, "parallelism": "single GPU"},
         "store_GBps": round(store_gbps, 3), "load_GBps": round(load_gbps, 3),
         "restore_s_128k": round(restore_128k, 4),
-        "restore_s_256k": None if restore_256k is None else round(restore_256k, 4),
+        "restore_s_256k": restore_256k,
         "restore_s_by_prefix_tokens": restore_by_len,
         "store_GBps_by_prefix_tokens": store_by_len,
         "spread": spread,
@@ -1230,7 +1440,10 @@ def main():
         "zero_copy_compare": zc,
         "restore_during_compute": overlap,
         "pool_alloc_s": round(alloc_s, 4),
-        "pool_alloc_s_256k": None if alloc_s_256k is None else round(alloc_s_256k, 4),
+        "leg_256k": leg256,
+        "pin_probe": pin_probe,
+        "timeline": timeline,
+        "device_leg": dleg,
         "staging_contiguous": bool(staging_contig),
         "parity": parity_msg if ok else f"FAILED: {parity_msg}",
         "parity_256k": parity_256k,

@@ -91,9 +91,13 @@ typedef int32_t kv_status;
 #define KV_MODE_ZERO_COPY 1u  /* gather/scatter kernels on `stream` access mapped pinned memory directly */
 #define KV_MODE_STAGED 2u     /* pack/unpack in device staging on `stream`; DMA copies on event-gated side streams */
 
-/* Pool host-memory kinds. */
+/* Pool memory kinds. */
 #define KV_HOST_COHERENT 0u     /* fine-grained pinned memory (default) */
 #define KV_HOST_NONCOHERENT 1u  /* coarse-grained pinned memory */
+#define KV_POOL_DEVICE 2u       /* device memory (HBM) of the current device, no host address: kv_store and
+                                   kv_load are then the pack/unpack kernels alone, device to device.  For a
+                                   device-resident chunk tier, the first hop of a peer (xGMI) exchange, and the
+                                   kernels' HBM roofline without the host link.  Zero-copy mode only. */
 
 /* Token order inside a cache block (kv_cache.block_order). */
 #define KV_BLOCK_HND 0  /* [2][H][BS][D] */
@@ -127,11 +131,12 @@ typedef struct kv_cache {
 /* Pool creation options.  Zero-initialised fields take the documented defaults. */
 typedef struct kv_pool_options {
     uint32_t mode;             /* KV_MODE_ZERO_COPY or KV_MODE_STAGED (required, no default) */
-    uint32_t host_kind;        /* KV_HOST_COHERENT (0) or KV_HOST_NONCOHERENT */
+    uint32_t host_kind;        /* KV_HOST_COHERENT (0), KV_HOST_NONCOHERENT or KV_POOL_DEVICE */
     int32_t staging_slots;     /* staged ring depth K >= 2 (default 3); with mode zero-copy, > 0
                                   also allocates staging so kv_pool_set_mode can switch later */
     int32_t chunks_per_batch;  /* chunks per staging slot / per kernel launch, 1..256 (default 16
-                                  staged, 256 zero-copy); applies to the mode given here */
+                                  staged and for a device pool, 256 zero-copy); applies to the mode
+                                  given here */
     int32_t side_streams;      /* staged: DMA side streams, 1..8 (default 2) */
     int32_t profile;           /* nonzero: time every pack/unpack launch (kv_pool_kernel_stats) */
     int64_t num_state_slots;   /* state-snapshot slots (0 = no state area) */
@@ -149,13 +154,14 @@ typedef struct kv_pool_info {
     int32_t device;
     uint32_t mode;             /* mode of stores (and of loads unless kv_pool_set_modes split them) */
     uint32_t host_kind;
-    int32_t is_pinned;         /* 1: the runtime reports the pool as pinned host memory */
+    int32_t is_pinned;         /* 1: the runtime reports the pool as pinned host memory (0 for a
+                                  KV_POOL_DEVICE pool) */
     int32_t staging_slots;
     int32_t chunks_per_batch;
     int32_t side_streams;
     int32_t staging_contiguous; /* always 0: staging is plain device memory (field kept for layout) */
-    void *host_base;           /* host address of slot 0 */
-    void *device_base;         /* device address of slot 0 (mapped pinned memory) */
+    void *host_base;           /* host address of slot 0 (NULL for a KV_POOL_DEVICE pool) */
+    void *device_base;         /* device address of slot 0 (mapped pinned memory, or HBM) */
     int64_t num_state_slots;
     int64_t state_slot_bytes;
     void *state_host_base;     /* host address of state slot 0 (NULL without a state area); the
@@ -183,7 +189,10 @@ typedef struct kv_state {
  * the current HIP device it creates the staging ring, side streams (default
  * priority, non-blocking) and events.  Never falls back to pageable memory:
  * failure is KV_ENOMEM.  *out receives the pool (owned by the library until
- * kv_pool_destroy).  Errors: KV_EINVAL (layout, num_slots <= 0, options),
+ * kv_pool_destroy).  With host_kind KV_POOL_DEVICE the same region is device
+ * memory of the current device instead (hipMalloc; is_pinned 0, no host
+ * address, kv_pool_slot returns NULL); the mode must be KV_MODE_ZERO_COPY and
+ * no staging is made.  Errors: KV_EINVAL (layout, num_slots <= 0, options),
  * KV_ENOMEM, KV_EHIP.
  */
 KV_API kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_pool_options *opts,

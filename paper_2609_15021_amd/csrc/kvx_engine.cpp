@@ -65,6 +65,8 @@ kv_status release(kv_pool *p) {
         note(hipHostFree(p->err_host), "hipHostFree(err)");
     if (p->host_base)
         note(hipHostFree(p->host_base), "hipHostFree(pool)");
+    if (p->on_device && p->dev_base)
+        note(hipFree(p->dev_base), "hipFree(device pool)");
     delete p;
     return first;
 }
@@ -257,7 +259,7 @@ kv_status transfer(kv_pool *p, const kv_cache *cache, const int32_t *block_table
         for (int64_t c0 = 0; c0 < nc; c0 += p->zc_chunks) {
             const int n = static_cast<int>(std::min<int64_t>(p->zc_chunks, nc - c0));
             kv_status st = enqueue_gather(p, cache, block_table, n_tokens, dir, c0, n, slots.data() + c0,
-                                          p->dev_base, g.slot_bytes, true, stream);
+                                          p->dev_base, g.slot_bytes, !p->on_device, stream);
             if (st != KV_OK)
                 return st;
         }
@@ -359,8 +361,8 @@ kv_status transfer_state(kv_pool *p, const kv_state *st, const int64_t *pages, i
     if (p->mode_of[dir] == KV_MODE_ZERO_COPY) {
         const StatePlan plan(st, n, kvx::kStatePiece);
         auto off = [&](int64_t k) { return slot_ids[k] * S; };
-        return enqueue_state(p, st, plan, pages, 0, plan.pieces, p->dev_base + p->state_offset, off, true, stream,
-                             dir);
+        return enqueue_state(p, st, plan, pages, 0, plan.pieces, p->dev_base + p->state_offset, off, !p->on_device,
+                             stream, dir);
     }
 
     // Staged mode: cut the pieces into batches of at most one staging slot of bytes.
@@ -485,15 +487,23 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
                              static_cast<long long>(num_slots));
         if (opts->mode != KV_MODE_ZERO_COPY && opts->mode != KV_MODE_STAGED)
             return kvx::fail(KV_EINVAL, "opts->mode must be KV_MODE_ZERO_COPY or KV_MODE_STAGED (got %u)", opts->mode);
-        if (opts->host_kind != KV_HOST_COHERENT && opts->host_kind != KV_HOST_NONCOHERENT)
+        if (opts->host_kind != KV_HOST_COHERENT && opts->host_kind != KV_HOST_NONCOHERENT &&
+            opts->host_kind != KV_POOL_DEVICE)
             return kvx::fail(KV_EINVAL, "unknown host_kind %u", opts->host_kind);
+        const bool on_device = opts->host_kind == KV_POOL_DEVICE;
+        if (on_device && (opts->mode != KV_MODE_ZERO_COPY || opts->staging_slots != 0))
+            return kvx::fail(KV_EINVAL, "a device pool (KV_POOL_DEVICE) takes KV_MODE_ZERO_COPY and no staging");
         // chunks_per_batch applies to the mode chosen at creation; the other mode keeps its default.
         if (opts->chunks_per_batch < 0 || opts->chunks_per_batch > kvx::kMaxLaunchChunks)
             return kvx::fail(KV_EINVAL, "chunks_per_batch must be in [1, %d] (got %d)", kvx::kMaxLaunchChunks,
                              opts->chunks_per_batch);
         const bool staged = opts->mode == KV_MODE_STAGED;
         const int cpb = (staged && opts->chunks_per_batch) ? opts->chunks_per_batch : kDefaultChunksPerBatch;
-        const int zc_chunks = (!staged && opts->chunks_per_batch) ? opts->chunks_per_batch : kvx::kMaxLaunchChunks;
+        // Zero-copy launches into host memory default to the largest launch (they stride a capped grid);
+        // device-pool launches default to the staged launch shape (one workgroup per slab).
+        const int zc_chunks = (!staged && opts->chunks_per_batch) ? opts->chunks_per_batch
+                              : on_device                        ? kDefaultChunksPerBatch
+                                                                 : kvx::kMaxLaunchChunks;
         const bool want_staging = opts->mode == KV_MODE_STAGED || opts->staging_slots > 0;
         const int K = opts->staging_slots ? opts->staging_slots : kDefaultStagingSlots;
         if (want_staging && (K < 2 || K > 64))
@@ -548,38 +558,56 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
             if (e != hipSuccess)
                 return bail(kvx::hip_fail(e, "hipGetDevice", __FILE__, __LINE__));
 
-            // One pinned, mapped region of exactly region_bytes (Sec. 3.3: no rounding allocator,
-            // and never a silent fallback to pageable memory).
-            const unsigned flags = hipHostMallocMapped | hipHostMallocPortable |
-                                   (p->host_kind == KV_HOST_COHERENT ? hipHostMallocCoherent
-                                                                     : hipHostMallocNonCoherent);
-            const auto t0 = std::chrono::steady_clock::now();
-            void *host = nullptr;
-            e = hipHostMalloc(&host, static_cast<size_t>(region_bytes), flags);
-            const auto t1 = std::chrono::steady_clock::now();
-            if (e != hipSuccess || !host) {
-                (void)hipGetLastError();
-                const long long want = static_cast<long long>(region_bytes);
-                release(p);
-                return kvx::fail(KV_ENOMEM, "pinned allocation of %lld bytes failed (%s); no pageable fallback", want,
-                                 hipGetErrorName(e));
-            }
-            p->host_base = static_cast<uint8_t *>(host);
-            p->alloc_seconds = std::chrono::duration<double>(t1 - t0).count();
+            if (on_device) {
+                // The device-resident tier: one plain allocation of exactly region_bytes.
+                p->on_device = true;
+                const auto t0 = std::chrono::steady_clock::now();
+                void *dptr = nullptr;
+                e = hipMalloc(&dptr, static_cast<size_t>(region_bytes));
+                const auto t1 = std::chrono::steady_clock::now();
+                if (e != hipSuccess || !dptr) {
+                    (void)hipGetLastError();
+                    const long long want = static_cast<long long>(region_bytes);
+                    release(p);
+                    return kvx::fail(KV_ENOMEM, "device allocation of %lld bytes for the pool failed (%s)", want,
+                                     hipGetErrorName(e));
+                }
+                p->dev_base = static_cast<uint8_t *>(dptr);
+                p->alloc_seconds = std::chrono::duration<double>(t1 - t0).count();
+            } else {
+                // One pinned, mapped region of exactly region_bytes (Sec. 3.3: no rounding allocator,
+                // and never a silent fallback to pageable memory).
+                const unsigned flags = hipHostMallocMapped | hipHostMallocPortable |
+                                       (p->host_kind == KV_HOST_COHERENT ? hipHostMallocCoherent
+                                                                         : hipHostMallocNonCoherent);
+                const auto t0 = std::chrono::steady_clock::now();
+                void *host = nullptr;
+                e = hipHostMalloc(&host, static_cast<size_t>(region_bytes), flags);
+                const auto t1 = std::chrono::steady_clock::now();
+                if (e != hipSuccess || !host) {
+                    (void)hipGetLastError();
+                    const long long want = static_cast<long long>(region_bytes);
+                    release(p);
+                    return kvx::fail(KV_ENOMEM, "pinned allocation of %lld bytes failed (%s); no pageable fallback",
+                                     want, hipGetErrorName(e));
+                }
+                p->host_base = static_cast<uint8_t *>(host);
+                p->alloc_seconds = std::chrono::duration<double>(t1 - t0).count();
 
-            hipPointerAttribute_t attr;
-            std::memset(&attr, 0, sizeof(attr));
-            e = hipPointerGetAttributes(&attr, host);
-            if (e != hipSuccess)
-                return bail(kvx::hip_fail(e, "hipPointerGetAttributes(pool)", __FILE__, __LINE__));
-            p->pinned = attr.type == hipMemoryTypeHost;
-            if (!p->pinned)
-                return bail(kvx::fail(KV_ENOMEM, "pool memory is not reported as pinned host memory"));
-            void *dptr = nullptr;
-            e = hipHostGetDevicePointer(&dptr, host, 0);
-            if (e != hipSuccess)
-                return bail(kvx::hip_fail(e, "hipHostGetDevicePointer(pool)", __FILE__, __LINE__));
-            p->dev_base = static_cast<uint8_t *>(dptr);
+                hipPointerAttribute_t attr;
+                std::memset(&attr, 0, sizeof(attr));
+                e = hipPointerGetAttributes(&attr, host);
+                if (e != hipSuccess)
+                    return bail(kvx::hip_fail(e, "hipPointerGetAttributes(pool)", __FILE__, __LINE__));
+                p->pinned = attr.type == hipMemoryTypeHost;
+                if (!p->pinned)
+                    return bail(kvx::fail(KV_ENOMEM, "pool memory is not reported as pinned host memory"));
+                void *dptr = nullptr;
+                e = hipHostGetDevicePointer(&dptr, host, 0);
+                if (e != hipSuccess)
+                    return bail(kvx::hip_fail(e, "hipHostGetDevicePointer(pool)", __FILE__, __LINE__));
+                p->dev_base = static_cast<uint8_t *>(dptr);
+            }
 
             e = hipHostMalloc(reinterpret_cast<void **>(&p->err_host), 256,
                               hipHostMallocMapped | hipHostMallocCoherent);
@@ -669,19 +697,20 @@ kv_status kv_pool_get_info(const kv_pool *pool, kv_pool_info *info) {
         info->device_base = pool->dev_base;
         info->num_state_slots = pool->num_state_slots;
         info->state_slot_bytes = pool->state_slot_bytes;
-        info->state_host_base = pool->num_state_slots > 0 ? pool->host_base + pool->state_offset : nullptr;
+        info->state_host_base =
+            pool->num_state_slots > 0 && pool->host_base ? pool->host_base + pool->state_offset : nullptr;
         return KV_OK;
     });
 }
 
 void *kv_pool_state_slot(kv_pool *pool, int64_t slot) {
-    if (!pool || slot < 0 || slot >= pool->num_state_slots)
+    if (!pool || !pool->host_base || slot < 0 || slot >= pool->num_state_slots)
         return nullptr;
     return pool->host_base + pool->state_offset + slot * pool->state_slot_bytes;
 }
 
 void *kv_pool_slot(kv_pool *pool, int64_t slot) {
-    if (!pool || slot < 0 || slot >= pool->num_slots)
+    if (!pool || !pool->host_base || slot < 0 || slot >= pool->num_slots)
         return nullptr;
     return pool->host_base + slot * pool->geo.slot_bytes;
 }

@@ -140,8 +140,9 @@ struct kv_pool {
     int device = 0;
     uint32_t mode_of[2] = {0, 0};     // transfer mode per direction: [kPack] stores, [kUnpack] loads
     uint32_t host_kind = 0;
-    uint8_t *host_base = nullptr;   // host address of slot 0
+    uint8_t *host_base = nullptr;   // host address of slot 0 (nullptr for a device pool)
     uint8_t *dev_base = nullptr;    // device address of slot 0
+    bool on_device = false;         // KV_POOL_DEVICE: the region is device memory (HBM)
     int32_t *err_host = nullptr;    // async error word (pinned, mapped)
     int32_t *err_dev = nullptr;
     double alloc_seconds = 0.0;

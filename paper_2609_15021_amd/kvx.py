@@ -31,6 +31,7 @@ KV_MODE_ZERO_COPY = 1
 KV_MODE_STAGED = 2
 KV_HOST_COHERENT = 0
 KV_HOST_NONCOHERENT = 1
+KV_POOL_DEVICE = 2
 KV_ASYNC_BAD_BLOCK = 1
 KV_BLOCK_HND = 0
 KV_BLOCK_NHD = 1
@@ -306,6 +307,8 @@ def kv_pool_kernel_stats(pool: Pool, which: str, reset: bool = False):
 def pool_view(pool: Pool) -> np.ndarray:
     """The whole pinned pool as a host uint8 numpy array (touch only when no call is in flight)."""
     info = kv_pool_get_info(pool)
+    if not info["host_base"]:
+        raise ValueError("a device pool (KV_POOL_DEVICE) has no host address")
     buf = (ctypes.c_uint8 * info["pool_bytes"]).from_address(info["host_base"])
     return np.ctypeslib.as_array(buf)
 

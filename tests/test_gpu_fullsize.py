@@ -46,8 +46,6 @@ def _blocks_equal(A, btA, B, btB, nblk, step=512):
 @pytest.mark.parametrize("n,NB", [(32768, 2560), (131072, 10240), (262336, 20480)],
                          ids=["32k", "128k", "256k+192"])
 def test_fullsize_store_load(mode, n, NB):
-    if mode == "zero_copy" and n > 131072:
-        pytest.skip("zero-copy 256k covered by the staged run's layout; keeps the suite short")
     lay = B27
     nblk, nc = lay.nblk(n), lay.nc(n)
     seed = harness.sub_seed("fullsize", n)

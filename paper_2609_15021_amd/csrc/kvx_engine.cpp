@@ -24,6 +24,50 @@
 using kvx::Direction;
 using kvx::Geometry;
 
+namespace kvx {
+
+hipError_t launch_gathers(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, Direction dir,
+                          int64_t chunk0, int nchunks, const int32_t *slots, uint8_t *chunk_base, int64_t slot_stride,
+                          bool host_side, int32_t *err, hipStream_t stream) {
+    const Geometry g = geometry(cache->layout, cache->block_stride_bytes);
+    for (int layer0 = 0; layer0 < g.L; layer0 += kMaxLaunchLayers) {
+        const int nl = static_cast<int>(std::min<int64_t>(kMaxLaunchLayers, g.L - layer0));
+        const int per_launch = max_chunks_per_launch(g, nl);
+        for (int c0 = 0; c0 < nchunks; c0 += per_launch) {
+            const int nc = std::min(per_launch, nchunks - c0);
+            GatherArgs a;
+            std::memset(&a, 0, sizeof(a));
+            for (int l = 0; l < nl; ++l)
+                a.layer[l] = static_cast<uint8_t *>(cache->layer_ptrs[layer0 + l]);
+            a.chunk_base = chunk_base;
+            a.block_table = block_table;
+            a.err = err;
+            a.slot_stride = slot_stride;
+            a.block_stride = g.block_stride;
+            a.n_tokens = n_tokens;
+            a.chunk0 = chunk0 + c0;
+            a.num_blocks = cache->num_blocks;
+            a.layer0 = layer0;
+            a.nlayers = nl;
+            a.H = static_cast<int32_t>(g.H);
+            a.BS = static_cast<int32_t>(g.BS);
+            a.C = static_cast<int32_t>(g.C);
+            a.vec_per_row = static_cast<int32_t>(g.vec_per_row);
+            a.blocks_per_chunk = static_cast<int32_t>(g.blocks_per_chunk);
+            a.nchunks = nc;
+            a.nhd = cache->block_order == KV_BLOCK_NHD ? 1 : 0;
+            for (int c = 0; c < nc; ++c)
+                a.slot[c] = slots[c0 + c];
+            const hipError_t e = launch_gather(a, dir, host_side, stream);
+            if (e != hipSuccess)
+                return e;
+        }
+    }
+    return hipSuccess;
+}
+
+}  // namespace kvx
+
 namespace {
 
 constexpr int kDefaultStagingSlots = 3;
@@ -102,7 +146,6 @@ kv_status enqueue_gather(kv_pool *p, const kv_cache *cache, const int32_t *block
                          Direction dir, int64_t chunk0, int nchunks, const int32_t *slots, uint8_t *chunk_base,
                          int64_t slot_stride, bool host_side, hipStream_t stream) {
     const Geometry &g0 = p->geo;
-    const Geometry g = kvx::geometry(cache->layout, cache->block_stride_bytes);
     hipEvent_t t_start = nullptr, t_stop = nullptr;
     if (p->profile) {
         kv_status st = take_timing_event(p, &t_start);
@@ -114,37 +157,8 @@ kv_status enqueue_gather(kv_pool *p, const kv_cache *cache, const int32_t *block
         KVX_HIP(hipEventRecord(t_start, stream));
     }
     int64_t payload = 0;
-    for (int layer0 = 0; layer0 < g.L; layer0 += kvx::kMaxLaunchLayers) {
-        const int nl = static_cast<int>(std::min<int64_t>(kvx::kMaxLaunchLayers, g.L - layer0));
-        const int per_launch = kvx::max_chunks_per_launch(g, nl);
-        for (int c0 = 0; c0 < nchunks; c0 += per_launch) {
-            const int nc = std::min(per_launch, nchunks - c0);
-            kvx::GatherArgs a;
-            std::memset(&a, 0, sizeof(a));
-            for (int l = 0; l < nl; ++l)
-                a.layer[l] = static_cast<uint8_t *>(cache->layer_ptrs[layer0 + l]);
-            a.chunk_base = chunk_base;
-            a.block_table = block_table;
-            a.err = p->err_dev;
-            a.slot_stride = slot_stride;
-            a.block_stride = g.block_stride;
-            a.n_tokens = n_tokens;
-            a.chunk0 = chunk0 + c0;
-            a.num_blocks = cache->num_blocks;
-            a.layer0 = layer0;
-            a.nlayers = nl;
-            a.H = static_cast<int32_t>(g.H);
-            a.BS = static_cast<int32_t>(g.BS);
-            a.C = static_cast<int32_t>(g.C);
-            a.vec_per_row = static_cast<int32_t>(g.vec_per_row);
-            a.blocks_per_chunk = static_cast<int32_t>(g.blocks_per_chunk);
-            a.nchunks = nc;
-            a.nhd = cache->block_order == KV_BLOCK_NHD ? 1 : 0;
-            for (int c = 0; c < nc; ++c)
-                a.slot[c] = slots[c0 + c];
-            KVX_HIP(kvx::launch_gather(a, dir, host_side, stream));
-        }
-    }
+    KVX_HIP(kvx::launch_gathers(cache, block_table, n_tokens, dir, chunk0, nchunks, slots, chunk_base, slot_stride,
+                                host_side, p->err_dev, stream));
     for (int c = 0; c < nchunks; ++c) {
         const int64_t i = chunk0 + c;
         const int64_t r = std::min<int64_t>(g0.C, n_tokens - i * g0.C);

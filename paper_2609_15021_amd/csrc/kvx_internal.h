@@ -88,6 +88,13 @@ hipError_t launch_gather(const GatherArgs &args, Direction dir, bool host_side, 
 // Largest chunk count per launch that keeps the grid within the 32-bit work-item limit.
 int max_chunks_per_launch(const Geometry &g, int nlayers);
 
+// Enqueue the pack/unpack launches for chunks [chunk0, chunk0 + nchunks) of a prefix of `cache`
+// (layers split over launches of at most kMaxLaunchLayers): slots[c] is the slot of chunk
+// chunk0 + c at chunk_base, slot_stride bytes apart.  No host allocation, no event.
+hipError_t launch_gathers(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens, Direction dir,
+                          int64_t chunk0, int nchunks, const int32_t *slots, uint8_t *chunk_base, int64_t slot_stride,
+                          bool host_side, int32_t *err, hipStream_t stream);
+
 // Thread-local error reporting.
 kv_status fail(kv_status code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 kv_status hip_fail(hipError_t err, const char *what, const char *file, int line);

@@ -301,6 +301,23 @@ KV_API kv_status kv_load(const kv_cache *cache, const int32_t *block_table, int6
                   const int64_t *chunk_ids, void *stream);
 
 /*
+ * kv_load_noalloc -- kv_load for callers that cannot allocate: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  Same arguments, result, ordering
+ * contract and argument errors as kv_load, for a host pool in either mode.  It allocates
+ * nothing: no hipMalloc/hipFree, no stream, no event, no host heap memory.  Each batch of
+ * chunks is copied from the pool into the library's static device scratch of
+ * KV_NOALLOC_SCRATCH_BYTES with hipMemcpyAsync and unpacked from there, every copy and kernel
+ * on `stream` in order.  The first call on a device looks up that device's scratch address.
+ * Limits: KV_EUNSUPPORTED if one chunk (C*TB bytes) exceeds the scratch; KV_EINVAL for a
+ * KV_POOL_DEVICE pool.  Every call on one GPU uses that GPU's one scratch array: calls that
+ * overlap on one GPU (on two streams at once) race, and the caller must order them.
+ * kv_pool_destroy does not wait for these calls: synchronise `stream` first.
+ */
+#define KV_NOALLOC_SCRATCH_BYTES ((int64_t)64 << 20)
+KV_API kv_status kv_load_noalloc(const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
+                                 kv_pool *pool, const int64_t *chunk_ids, void *stream);
+
+/*
  * Host-only validation of a state-snapshot request, no HIP call.  Checks:
  * G >= 1; page_bytes >= 1; page_stride 0 or >= page_bytes; num_pages >= 1;
  * G*page_bytes == pool_state_slot_bytes (the pool's snapshot format); n >= 0;

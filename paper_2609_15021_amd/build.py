@@ -26,7 +26,8 @@ NO_PACKED_FP32 = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wextra",
           "-Wno-unused-parameter", *NO_PACKED_FP32]
 
-KVX_SOURCES = ["kvx_check.cpp", "kvx_engine.cpp", "kvx_gather.hip", "kvx_state.hip", "kvx_index.cpp", "kvx_tier.cpp"]
+KVX_SOURCES = ["kvx_check.cpp", "kvx_engine.cpp", "kvx_gather.hip", "kvx_state.hip", "kvx_index.cpp", "kvx_tier.cpp",
+               "kvx_noalloc.hip"]
 
 
 def _run(cmd, verbose):

@@ -119,6 +119,7 @@ def _open():
         "kv_check": ([ctypes.POINTER(KvCache), ctypes.POINTER(KvLayout), i64, i64, P, ctypes.c_int], i32),
         "kv_store": ([ctypes.POINTER(KvCache), P, i64, P, P, P], i32),
         "kv_load": ([ctypes.POINTER(KvCache), P, i64, P, P, P], i32),
+        "kv_load_noalloc": ([ctypes.POINTER(KvCache), P, i64, P, P, P], i32),
         "kv_pool_state_slot": ([P, i64], P),
         "kv_check_state": ([ctypes.POINTER(KvState), i64, i64, i64, P, P, ctypes.c_int], i32),
         "kv_store_state": ([ctypes.POINTER(KvState), P, i64, P, P, P], i32),
@@ -160,7 +161,8 @@ _lib = _open()
 EXPORTS = ("kv_pool_create", "kv_pool_destroy", "kv_pool_get_info", "kv_pool_slot", "kv_pool_slot_bytes",
            "kv_pool_num_slots", "kv_pool_set_mode", "kv_pool_set_modes", "kv_pool_async_error",
            "kv_pool_kernel_stats", "kv_check",
-           "kv_store", "kv_load", "kv_last_error", "kv_status_name", "kv_version", "kv_pool_state_slot",
+           "kv_store", "kv_load", "kv_load_noalloc", "kv_last_error", "kv_status_name", "kv_version",
+           "kv_pool_state_slot",
            "kv_check_state", "kv_store_state", "kv_load_state", "kv_index_create", "kv_index_destroy",
            "kv_index_keys", "kv_index_lookup", "kv_index_unpin", "kv_index_reserve", "kv_index_commit",
            "kv_index_reserve_state", "kv_index_commit_state", "kv_index_get_stats", "kv_ipc_export", "kv_ipc_check",
@@ -461,6 +463,16 @@ def kv_load(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, str
     _check_lengths(cache.layout, n_tokens, ids.size, _table_len(block_table))
     _raise(_lib.kv_load(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
                         pool.handle, ptr, _stream_handle(stream)))
+    if block_table is not None and int(n_tokens) > 0:
+        _in_use_on(block_table, stream)
+
+
+def kv_load_noalloc(cache: Cache, block_table, n_tokens: int, pool: Pool, chunk_ids, stream=None) -> None:
+    """kv_load through the library's static device scratch: allocates nothing (see kvx.h)."""
+    ids, ptr = _chunk_ids(chunk_ids)
+    _check_lengths(cache.layout, n_tokens, ids.size, _table_len(block_table))
+    _raise(_lib.kv_load_noalloc(ctypes.byref(cache.struct), _block_table_ptr(block_table, cache), int(n_tokens),
+                                pool.handle, ptr, _stream_handle(stream)))
     if block_table is not None and int(n_tokens) > 0:
         _in_use_on(block_table, stream)
 

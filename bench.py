@@ -36,7 +36,7 @@ METRIC = "KV store/load GB/s and seconds to restore a 128k/256k-token prefix, 1 
 L, H, D, E, BS, C = 64, 8, 128, 2, 16, 256
 TOKEN_BYTES = 2 * L * H * D * E
 HBM_PEAK_GBPS = 8000.0
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "gather_pack_staged_128k_traffic.txt")
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "gather_device_128k_traffic.txt")
 GATHER_SRC = os.path.join(ROOT, "paper_2609_15021_amd", "csrc", "kvx_gather.hip")
 
 
@@ -446,6 +446,33 @@ def tier_store(np, torch, harness, hg, kvx, sock, dev):
     dt = time.perf_counter() - t0
     c.close()
     print(json.dumps({"store_s": dt, "stored_chunks": stored}), flush=True)
+    sys.stdin.read()  # a live replica: keep running (and holding the cache) until the bench is done with B
+
+
+def start_replica(flag, sock, timeout=300):
+    """Replica A in its own process: it stores through the tier, prints its result and stays alive,
+    holding its cache, until its stdin closes.  Both replicas of the paper are long-lived; a replica
+    process that exited right after its store would free tens of GiB of device memory just before B's
+    restore, and the driver's clearing of freed device memory slows DMA copies for seconds (128k
+    restores measured 0.742 s instead of 0.603 s after a 32 GiB free).  Returns (process, result)."""
+    import select
+    import subprocess
+    proc = subprocess.Popen([sys.executable, "-u", os.path.abspath(__file__), flag, sock], stdin=subprocess.PIPE,
+                            stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+    ready, _, _ = select.select([proc.stdout], [], [], timeout)
+    line = proc.stdout.readline() if ready else ""
+    if not line.startswith("{"):
+        proc.kill()
+        raise RuntimeError("replica A failed: " + (line + proc.stderr.read())[-2000:])
+    return proc, json.loads(line)
+
+
+def stop_replica(proc):
+    proc.stdin.close()
+    try:
+        proc.wait(timeout=60)
+    except Exception:
+        proc.kill()
 
 
 def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
@@ -465,11 +492,7 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
         line = tier.stdout.readline()
         if not line.startswith("READY"):
             raise RuntimeError("tier did not start: " + tier.stderr.read()[-2000:])
-        r = subprocess.run([sys.executable, "-u", me, "--tier-store", sock], capture_output=True, text=True,
-                           timeout=300)
-        if r.returncode != 0:
-            raise RuntimeError("replica A failed: " + r.stderr[-2000:])
-        a_out = json.loads(r.stdout.strip().splitlines()[-1])
+        rep_a, a_out = start_replica("--tier-store", sock)
         store_s = a_out["store_s"]
         seed = harness.sub_seed("bench-tier", TIER_N)
         layers_b, cache_b = layer_caches(torch, hg, kvx, TIER_NB, dev)
@@ -484,6 +507,7 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
             hits.append(kvx.kv_tier_load_prefix(c.fileno(), cache_b, bt_b, 1, prompt))
             restore.append(time.perf_counter() - t0)
         c.close()
+        stop_replica(rep_a)
         out, err = tier.communicate(timeout=120)
         if tier.returncode != 0:
             raise RuntimeError("tier failed: " + (out + err)[-2000:])
@@ -577,6 +601,7 @@ def paper_hybrid_store(torch, harness, hg, kvx, sock, dev):
     dt = time.perf_counter() - t0
     c.close()
     print(json.dumps({"store_s": dt, "stored_chunks": stored, "stored_state": stored_state}), flush=True)
+    sys.stdin.read()  # a live replica: keep running (and holding the cache) until the bench is done with B
 
 
 def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
@@ -593,11 +618,7 @@ def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=N
     try:
         if not tier.stdout.readline().startswith("READY"):
             raise RuntimeError("tier did not start: " + tier.stderr.read()[-2000:])
-        r = subprocess.run([sys.executable, "-u", me, "--paper-hybrid-store", sock], capture_output=True, text=True,
-                           timeout=300)
-        if r.returncode != 0:
-            raise RuntimeError("replica A failed: " + r.stderr[-2000:])
-        a_out = json.loads(r.stdout.strip().splitlines()[-1])
+        rep_a, a_out = start_replica("--paper-hybrid-store", sock)
         seed = harness.sub_seed("bench-paper-hybrid")
         layers_b, pages_b, cache_b, state_b = paper_hybrid_cache(torch, hg, kvx, dev)
         nblk = -(-PH["N"] // PH["BS"])
@@ -612,6 +633,7 @@ def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=N
             hits.append(kvx.kv_tier_load_prefix(c.fileno(), cache_b, bt_b, 3, prompt, state=state_b, state_page=0))
             restore.append(time.perf_counter() - t0)
         c.close()
+        stop_replica(rep_a)
         out, err = tier.communicate(timeout=120)
         if tier.returncode != 0:
             raise RuntimeError("tier failed: " + (out + err)[-2000:])
@@ -934,6 +956,7 @@ def concurrent_leg(torch, kvx, rep_a, rep_b, t_a, t_b, n, ids, pool, reps=3):
     sb, lb = m * TOKEN_BYTES, (n - m) * TOKEN_BYTES
     return {"bytes_per_direction": sb, "seconds": round(statistics.median(walls), 4),
             "aggregate_GBps": round((sb + lb) / statistics.median(walls) / 1e9, 2),
+            "aggregate_GBps_each": [round((sb + lb) / w / 1e9, 2) for w in walls],
             "store_GBps": round(sb / statistics.median(st) / 1e9, 2),
             "load_GBps": round(lb / statistics.median(ld) / 1e9, 2),
             "workload": f"store of tokens [0, {m:,}) from replica A and load of tokens [{m:,}, {n:,}) into "

@@ -132,12 +132,13 @@ typedef struct kv_cache {
 typedef struct kv_pool_options {
     uint32_t mode;             /* KV_MODE_ZERO_COPY or KV_MODE_STAGED (required, no default) */
     uint32_t host_kind;        /* KV_HOST_COHERENT (0), KV_HOST_NONCOHERENT or KV_POOL_DEVICE */
-    int32_t staging_slots;     /* staged ring depth K >= 2 (default 3); with mode zero-copy, > 0
-                                  also allocates staging so kv_pool_set_mode can switch later */
+    int32_t staging_slots;     /* staged ring depth K >= 2 per direction (default 3; stores and loads
+                                  each have their own ring); with mode zero-copy, > 0 also allocates
+                                  staging so kv_pool_set_mode can switch later */
     int32_t chunks_per_batch;  /* chunks per staging slot / per kernel launch, 1..256 (default 16
                                   staged and for a device pool, 256 zero-copy); applies to the mode
                                   given here */
-    int32_t side_streams;      /* staged: DMA side streams, 1..8 (default 2) */
+    int32_t side_streams;      /* staged: DMA side streams per direction, 1..8 (default 1) */
     int32_t profile;           /* nonzero: time every pack/unpack launch (kv_pool_kernel_stats) */
     int64_t num_state_slots;   /* state-snapshot slots (0 = no state area) */
     int64_t state_slot_bytes;  /* bytes of one state slot = G*page_bytes, a multiple of 16 (0 if none) */
@@ -149,7 +150,7 @@ typedef struct kv_pool_info {
     int64_t num_slots;
     int64_t slot_bytes;        /* C * TB */
     int64_t pool_bytes;        /* num_slots * slot_bytes, pinned as one region */
-    int64_t staging_bytes;     /* device staging (0 without staging) */
+    int64_t staging_bytes;     /* device staging of both directions (0 without staging) */
     double alloc_seconds;      /* wall time of the pinned allocation (cf. Sec. 3.3) */
     int32_t device;
     uint32_t mode;             /* mode of stores (and of loads unless kv_pool_set_modes split them) */
@@ -186,8 +187,9 @@ typedef struct kv_state {
  * Pins exactly num_slots * slot_bytes bytes as ONE region (Sec. 3.2 notes a
  * workaround registering the whole pool together), mapped for device access,
  * verifies with the runtime that it is pinned, and times the allocation.  On
- * the current HIP device it creates the staging ring, side streams (default
- * priority, non-blocking) and events.  Never falls back to pageable memory:
+ * the current HIP device it creates, for stores and for loads separately, a
+ * staging ring, side streams (default priority, non-blocking) and events, so
+ * that a store and a load in flight at once do not wait for each other.  Never falls back to pageable memory:
  * failure is KV_ENOMEM.  *out receives the pool (owned by the library until
  * kv_pool_destroy).  With host_kind KV_POOL_DEVICE the same region is device
  * memory of the current device instead (hipMalloc; is_pinned 0, no host

@@ -12,7 +12,9 @@
 //    the caller's stream waits for its copy;
 //  * staging slot k is reused only after the event of its last use (copy or unpack)
 //    completed -- premature reuse of an asynchronous-copy buffer is the related failure
-//    the paper cites (Sec. 3.2).
+//    the paper cites (Sec. 3.2);
+//  * stores and loads each have their own lane (staging ring, side streams, events), so a
+//    store and a load in flight at once use the host link in both directions.
 // No call ever blocks the host on device work.
 #include <algorithm>
 #include <chrono>
@@ -72,7 +74,9 @@ namespace {
 
 constexpr int kDefaultStagingSlots = 3;
 constexpr int kDefaultChunksPerBatch = 16;
-constexpr int kDefaultSideStreams = 2;
+// One DMA side stream per direction: a store and a load in flight at once then move ~99 GB/s in total
+// (two per direction measured 57-64 GB/s: the runtime spreads their copies over more copy engines).
+constexpr int kDefaultSideStreams = 1;
 
 kv_status release(kv_pool *p) {
     // Best-effort teardown: keep going after a failure, report the first one.
@@ -86,15 +90,17 @@ kv_status release(kv_pool *p) {
         note(hipEventSynchronize(use.second), "hipEventSynchronize(last use)");
     for (auto &use : p->last_use)
         note(hipEventDestroy(use.second), "hipEventDestroy");
-    for (hipStream_t s : p->sides)
-        note(hipStreamSynchronize(s), "hipStreamSynchronize(side)");
-    for (hipStream_t s : p->sides)
-        note(hipStreamDestroy(s), "hipStreamDestroy");
-    for (auto *vec : {&p->ev_free, &p->ev_ready, &p->ev_join})
-        for (hipEvent_t e : *vec)
-            note(hipEventDestroy(e), "hipEventDestroy");
-    if (p->ev_entry)
-        note(hipEventDestroy(p->ev_entry), "hipEventDestroy");
+    for (auto &lane : p->lane) {
+        for (hipStream_t s : lane.sides)
+            note(hipStreamSynchronize(s), "hipStreamSynchronize(side)");
+        for (hipStream_t s : lane.sides)
+            note(hipStreamDestroy(s), "hipStreamDestroy");
+        for (auto *vec : {&lane.ev_free, &lane.ev_ready, &lane.ev_join})
+            for (hipEvent_t e : *vec)
+                note(hipEventDestroy(e), "hipEventDestroy");
+        if (lane.ev_entry)
+            note(hipEventDestroy(lane.ev_entry), "hipEventDestroy");
+    }
     for (int w = 0; w < 4; ++w)
         for (auto &t : p->pending[w]) {
             note(hipEventSynchronize(t.stop), "hipEventSynchronize");
@@ -193,69 +199,70 @@ void add_run(std::vector<Run> &runs, int64_t host_off, int64_t stage_off, int64_
 using BatchRuns = std::function<void(int64_t batch, std::vector<Run> &runs)>;
 using BatchKernels = std::function<kv_status(int64_t batch, uint8_t *stage)>;
 
-// The staged pipeline over `nbatches` batches, each filling at most one staging slot.
-// Store: kernels on the caller's stream pack batch b into staging slot k (after the copy
-// that last read slot k), then a side stream copies it to the pool; the caller's stream
-// finally waits for every side stream (exit join).  Load: an entry event on the caller's
-// stream gates the side streams' pool reads; each batch's kernels wait for its copy.
+// The staged pipeline over `nbatches` batches, each filling at most one staging slot of the
+// direction's own lane.  Store: kernels on the caller's stream pack batch b into staging slot k
+// (after the copy that last read slot k), then a side stream copies it to the pool; the caller's
+// stream finally waits for every side stream it used (exit join).  Load: an entry event on the
+// caller's stream gates the side streams' pool reads; each batch's kernels wait for its copy.
 kv_status staged_pipeline(kv_pool *p, int64_t nbatches, const BatchRuns &runs_of, const BatchKernels &kernels,
                           hipStream_t stream, Direction dir) {
+    kv_pool::Lane &ln = p->lane[dir];
     const int64_t staging_slot_bytes = static_cast<int64_t>(p->cpb) * p->geo.slot_bytes;
-    std::vector<bool> side_used(p->sides.size(), false);
+    std::vector<bool> side_used(ln.sides.size(), false);
     std::vector<Run> runs;
 
     if (dir == kvx::kUnpack)
-        KVX_HIP(hipEventRecord(p->ev_entry, stream));  // entry gate for pool reads
+        KVX_HIP(hipEventRecord(ln.ev_entry, stream));  // entry gate for pool reads
 
     for (int64_t b = 0; b < nbatches; ++b) {
-        const int k = p->ring;
-        p->ring = (p->ring + 1) % p->K;
-        const size_t si = static_cast<size_t>(b % static_cast<int64_t>(p->sides.size()));
-        hipStream_t side = p->sides[si];
-        uint8_t *stage = p->staging + static_cast<int64_t>(k) * staging_slot_bytes;
+        const int k = ln.ring;
+        ln.ring = (ln.ring + 1) % p->K;
+        const size_t si = static_cast<size_t>(b % static_cast<int64_t>(ln.sides.size()));
+        hipStream_t side = ln.sides[si];
+        uint8_t *stage = ln.staging + static_cast<int64_t>(k) * staging_slot_bytes;
         runs.clear();
         runs_of(b, runs);
 
         if (dir == kvx::kPack) {
-            if (p->free_recorded[k])
-                KVX_HIP(hipStreamWaitEvent(stream, p->ev_free[k], 0));
+            if (ln.free_recorded[k])
+                KVX_HIP(hipStreamWaitEvent(stream, ln.ev_free[k], 0));
             kv_status st = kernels(b, stage);
             if (st != KV_OK)
                 return st;
-            KVX_HIP(hipEventRecord(p->ev_ready[k], stream));
-            KVX_HIP(hipStreamWaitEvent(side, p->ev_ready[k], 0));
+            KVX_HIP(hipEventRecord(ln.ev_ready[k], stream));
+            KVX_HIP(hipStreamWaitEvent(side, ln.ev_ready[k], 0));
             for (const Run &run : runs)
                 KVX_HIP(hipMemcpyAsync(p->host_base + run.host_off, stage + run.stage_off,
                                        static_cast<size_t>(run.bytes), hipMemcpyDeviceToHost, side));
-            KVX_HIP(hipEventRecord(p->ev_free[k], side));
-            p->free_recorded[k] = true;
+            KVX_HIP(hipEventRecord(ln.ev_free[k], side));
+            ln.free_recorded[k] = true;
             side_used[si] = true;
         } else {
             if (!side_used[si]) {
-                KVX_HIP(hipStreamWaitEvent(side, p->ev_entry, 0));
+                KVX_HIP(hipStreamWaitEvent(side, ln.ev_entry, 0));
                 side_used[si] = true;
             }
-            if (p->free_recorded[k])
-                KVX_HIP(hipStreamWaitEvent(side, p->ev_free[k], 0));
+            if (ln.free_recorded[k])
+                KVX_HIP(hipStreamWaitEvent(side, ln.ev_free[k], 0));
             for (const Run &run : runs)
                 KVX_HIP(hipMemcpyAsync(stage + run.stage_off, p->host_base + run.host_off,
                                        static_cast<size_t>(run.bytes), hipMemcpyHostToDevice, side));
-            KVX_HIP(hipEventRecord(p->ev_ready[k], side));
-            KVX_HIP(hipStreamWaitEvent(stream, p->ev_ready[k], 0));
+            KVX_HIP(hipEventRecord(ln.ev_ready[k], side));
+            KVX_HIP(hipStreamWaitEvent(stream, ln.ev_ready[k], 0));
             kv_status st = kernels(b, stage);
             if (st != KV_OK)
                 return st;
-            KVX_HIP(hipEventRecord(p->ev_free[k], stream));
-            p->free_recorded[k] = true;
+            KVX_HIP(hipEventRecord(ln.ev_free[k], stream));
+            ln.free_recorded[k] = true;
         }
     }
     if (dir == kvx::kPack) {
         // Exit join: later work on the caller's stream follows every D2H copy.
-        for (size_t si = 0; si < p->sides.size(); ++si) {
+        for (size_t si = 0; si < ln.sides.size(); ++si) {
             if (!side_used[si])
                 continue;
-            KVX_HIP(hipEventRecord(p->ev_join[si], p->sides[si]));
-            KVX_HIP(hipStreamWaitEvent(stream, p->ev_join[si], 0));
+            KVX_HIP(hipEventRecord(ln.ev_join[si], ln.sides[si]));
+            KVX_HIP(hipStreamWaitEvent(stream, ln.ev_join[si], 0));
         }
     }
     return KV_OK;
@@ -636,40 +643,44 @@ kv_status kv_pool_create(const kv_layout *layout, int64_t num_slots, const kv_po
                 p->K = K;
                 p->cpb = cpb;
                 p->S = S;
-                const size_t staging_bytes = static_cast<size_t>(K) * cpb * static_cast<size_t>(p->geo.slot_bytes);
+                const size_t lane_bytes = static_cast<size_t>(K) * cpb * static_cast<size_t>(p->geo.slot_bytes);
                 // Plain device memory.  Physically contiguous staging (hipExtMallocWithFlags with
                 // hipDeviceMallocContiguous) was used before, but on MI355X with this runtime, once such
                 // an allocation had been freed, later allocations of the process read and wrote wrong
                 // bytes (156 of 480 seeded round trips in one process); plain staging measured the same
                 // transfer rates.
                 p->staging_contiguous = false;
-                e = hipMalloc(reinterpret_cast<void **>(&p->staging), staging_bytes);
+                e = hipMalloc(reinterpret_cast<void **>(&p->staging), 2 * lane_bytes);
                 if (e != hipSuccess)
                     return bail(kvx::hip_fail(e, "hipMalloc(staging)", __FILE__, __LINE__));
-                for (int s = 0; s < S; ++s) {
-                    hipStream_t side = nullptr;
-                    // Default priority on purpose: every stream of the library shares one priority.
-                    e = hipStreamCreateWithFlags(&side, hipStreamNonBlocking);
-                    if (e != hipSuccess)
-                        return bail(kvx::hip_fail(e, "hipStreamCreateWithFlags", __FILE__, __LINE__));
-                    p->sides.push_back(side);
-                    hipEvent_t j = nullptr;
-                    if ((st = make_event(&j, false)) != KV_OK)
+                for (int d = 0; d < 2; ++d) {
+                    kv_pool::Lane &ln = p->lane[d];
+                    ln.staging = p->staging + static_cast<size_t>(d) * lane_bytes;
+                    for (int s = 0; s < S; ++s) {
+                        hipStream_t side = nullptr;
+                        // Default priority on purpose: every stream of the library shares one priority.
+                        e = hipStreamCreateWithFlags(&side, hipStreamNonBlocking);
+                        if (e != hipSuccess)
+                            return bail(kvx::hip_fail(e, "hipStreamCreateWithFlags", __FILE__, __LINE__));
+                        ln.sides.push_back(side);
+                        hipEvent_t j = nullptr;
+                        if ((st = make_event(&j, false)) != KV_OK)
+                            return bail(st);
+                        ln.ev_join.push_back(j);
+                    }
+                    for (int k = 0; k < K; ++k) {
+                        hipEvent_t a = nullptr, b = nullptr;
+                        if ((st = make_event(&a, false)) != KV_OK)
+                            return bail(st);
+                        ln.ev_free.push_back(a);
+                        if ((st = make_event(&b, false)) != KV_OK)
+                            return bail(st);
+                        ln.ev_ready.push_back(b);
+                    }
+                    ln.free_recorded.assign(static_cast<size_t>(K), false);
+                    if ((st = make_event(&ln.ev_entry, false)) != KV_OK)
                         return bail(st);
-                    p->ev_join.push_back(j);
                 }
-                for (int k = 0; k < K; ++k) {
-                    hipEvent_t a = nullptr, b = nullptr;
-                    if ((st = make_event(&a, false)) != KV_OK)
-                        return bail(st);
-                    p->ev_free.push_back(a);
-                    if ((st = make_event(&b, false)) != KV_OK)
-                        return bail(st);
-                    p->ev_ready.push_back(b);
-                }
-                p->free_recorded.assign(static_cast<size_t>(K), false);
-                if ((st = make_event(&p->ev_entry, false)) != KV_OK)
-                    return bail(st);
             }
         } catch (...) {
             release(p);
@@ -696,7 +707,8 @@ kv_status kv_pool_get_info(const kv_pool *pool, kv_pool_info *info) {
         info->num_slots = pool->num_slots;
         info->slot_bytes = pool->geo.slot_bytes;
         info->pool_bytes = pool->pool_bytes;
-        info->staging_bytes = pool->staging ? static_cast<int64_t>(pool->K) * pool->cpb * pool->geo.slot_bytes : 0;
+        info->staging_bytes =
+            pool->staging ? 2 * static_cast<int64_t>(pool->K) * pool->cpb * pool->geo.slot_bytes : 0;
         info->alloc_seconds = pool->alloc_seconds;
         info->device = pool->device;
         info->mode = pool->mode_of[kvx::kPack];

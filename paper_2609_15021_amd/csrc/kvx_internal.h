@@ -155,17 +155,22 @@ struct kv_pool {
     double alloc_seconds = 0.0;
     bool pinned = false;
 
-    // Staging ring (staged mode).
-    int K = 0, cpb = 0, S = 0;
-    uint8_t *staging = nullptr;     // K slots of cpb*slot_bytes each
+    // Staged mode: one lane per direction, each with its own staging ring, DMA side streams and
+    // events, so a store and a load in flight at once never wait for each other's slots or streams.
+    struct Lane {
+        uint8_t *staging = nullptr;        // K slots of cpb*slot_bytes each
+        std::vector<hipStream_t> sides;    // DMA side streams of this direction
+        std::vector<hipEvent_t> ev_free;   // staging slot k may be overwritten once this completes
+        std::vector<bool> free_recorded;
+        std::vector<hipEvent_t> ev_ready;  // staging slot k holds the current batch
+        std::vector<hipEvent_t> ev_join;   // per side stream: exit join of a store
+        hipEvent_t ev_entry = nullptr;     // entry gate of a load
+        int ring = 0;
+    };
+    int K = 0, cpb = 0, S = 0;       // ring depth, chunks per slot, side streams: per direction
+    uint8_t *staging = nullptr;      // both lanes' staging (one allocation)
     bool staging_contiguous = false;  // always false: staging is plain device memory
-    std::vector<hipStream_t> sides;
-    std::vector<hipEvent_t> ev_free;   // staging slot k may be overwritten once this completes
-    std::vector<bool> free_recorded;
-    std::vector<hipEvent_t> ev_ready;  // staging slot k holds the current batch
-    std::vector<hipEvent_t> ev_join;   // per side stream: exit join of a store
-    hipEvent_t ev_entry = nullptr;     // entry gate of a load
-    int ring = 0;
+    Lane lane[2];                    // [kPack] stores, [kUnpack] loads
     int zc_chunks = 0;                 // chunks per zero-copy launch
     // Last use of the pool on each caller stream (recorded after every store/load), so that
     // kv_pool_destroy never frees memory that queued kernels or copies still touch.

@@ -384,7 +384,9 @@ def test_pool_info_and_errors():
     assert info["staging_contiguous"] == 0
     staged = kvx.kv_pool_create(lay.kv, 2, "staged", staging_slots=2, chunks_per_batch=1)
     sinfo = kvx.kv_pool_get_info(staged)
-    assert sinfo["staging_bytes"] == 2 * lay.slot_bytes and sinfo["staging_contiguous"] == 0
+    # One ring of 2 slots x 1 chunk per direction (stores and loads each have their own lane).
+    assert sinfo["staging_bytes"] == 2 * 2 * lay.slot_bytes and sinfo["staging_contiguous"] == 0
+    assert sinfo["side_streams"] == 1 and sinfo["staging_slots"] == 2
     kvx.kv_pool_destroy(staged)
     assert kvx.kv_pool_slot_bytes(pool) == lay.slot_bytes and kvx.kv_pool_num_slots(pool) == 4
     assert kvx.kv_pool_slot(pool, 3) == info["host_base"] + 3 * lay.slot_bytes

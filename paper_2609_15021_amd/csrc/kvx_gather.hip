@@ -21,7 +21,7 @@
 //
 // Index math is one division at thread start; afterwards every step is an addition with
 // carry.  Streaming data is read and written nontemporally.  Device-side (staged) launches
-// run one workgroup per slab and cap residency at 4 workgroups per CU (KVX_LDS_RESERVE).
+// run one workgroup per slab and cap residency at 5 workgroups per CU (KVX_LDS_RESERVE).
 // Host-side (zero-copy) launches run a few dozen workgroups that stride over the slabs
 // (KVX_HOST_WGS_*): the link bounds them, and the rest of the chip stays free.
 #include <algorithm>
@@ -48,11 +48,13 @@ typedef uint32_t vec16 __attribute__((ext_vector_type(4)));
 #define KVX_NT_STORE 1
 #endif
 // Dynamic LDS reserved per workgroup (never touched) to cap the workgroups resident per CU:
-// 40 KiB of the CU's 160 KiB allows 4 (16 waves per CU).  Measured on MI355X with the
-// 27B-class layout, 4 resident workgroups move slabs faster than 3 or than 6 and more:
-// fewer concurrent 32 KiB streams per CU keep the HBM read/write mix efficient.
+// 32 KiB of the CU's 160 KiB allows 5 (20 waves per CU).  Measured on MI355X with the
+// 27B-class layout, variants alternating on the same cache allocations in one process: 5
+// resident workgroups moved 4.2-4.6% more than 4 on two machines and the same on two others,
+// while 6, 7 and 8 lose on unpack (-2% to -5% against 4), as does an uncapped launch: fewer
+// concurrent 32 KiB streams per CU keep the HBM read/write mix efficient, too few leave HBM idle.
 #ifndef KVX_LDS_RESERVE
-#define KVX_LDS_RESERVE 40960
+#define KVX_LDS_RESERVE 32768
 #endif
 // Workgroups of a host-side (zero-copy) pack / unpack launch; each strides over the
 // launch's slabs (0: one workgroup per slab).  Measured on MI355X at the 27B-class layout

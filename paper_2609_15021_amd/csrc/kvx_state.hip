@@ -3,9 +3,9 @@
 // their device page buffers and the packed state slots, [G][page_bytes] per snapshot.
 //
 // Each page is contiguous on both sides, so the move is a batched copy: a workgroup moves
-// one piece (up to 64 KiB) of one page at a time with 16-byte vectors, every lane of a wave
-// touching consecutive vectors on both sides.  Device-side launches run one workgroup per
-// piece; host-side (zero-copy) launches run a few workgroups that stride over the pieces.
+// one piece (up to 64 KiB) of one page at a time with 16-byte vectors.  Device-side launches
+// run one workgroup per piece and pass it through LDS; host-side (zero-copy) launches run a
+// few workgroups that stride over the pieces and copy directly.
 // This work is bound by HBM (staging) or by
 // the host link (zero-copy); there is no arithmetic to put on the matrix cores.  Bytes
 // never pass through a float register.
@@ -19,8 +19,10 @@ namespace {
 
 typedef uint32_t svec16 __attribute__((ext_vector_type(4)));
 
-// Vectors each lane keeps in flight before storing.
+// Vectors each lane keeps in flight before storing (host-side launches).
 constexpr int kStateUnroll = 4;
+// LDS of a device-side workgroup: the buffer the piece passes through, 32 KiB at a time.
+constexpr int kStateLds = 32768;
 
 // Workgroups of a host-side (zero-copy) launch, striding over its pieces (0: one per piece).
 // Measured on MI355X with 16 x 48 pages of 3.06 MiB (store / load GB/s): one per piece
@@ -49,6 +51,33 @@ __device__ __forceinline__ void move_piece(const StateArgs &a, int64_t q) {
     const __amdgpu_buffer_rsrc_t dst_buf =
         __builtin_amdgcn_make_buffer_rsrc(dst, 0, static_cast<int>(len), 0x00020000);
 
+    if constexpr (!HOST_SIDE) {
+        // Device-side launches move the piece through LDS in 32 KiB halves: contiguous reads into
+        // LDS, then writes with each pass spread over 8 segments of the half (512 B each).  Paired on
+        // 48 x 3.06 MiB pages, this moved 2.8-4.5% more (pack) and 3.9-4.0% more (unpack) than the
+        // direct copy with 4 vectors in flight; the LDS reservation alone changed nothing.
+        extern __shared__ svec16 lds_half[];
+        constexpr int kHalf = kStateLds / 16, kPer = kThreads / 8;
+        const int tid = static_cast<int>(threadIdx.x);
+        for (int h0 = 0; h0 < nv; h0 += kHalf) {
+            const int hn = min(kHalf, nv - h0);
+            if (hn % (8 * kPer) != 0) {  // a short tail: straight copy
+                for (int v = h0 + tid; v < h0 + hn; v += kThreads)
+                    __builtin_nontemporal_store(__builtin_nontemporal_load(src + v), dst + v);
+                continue;
+            }
+            for (int v = tid; v < hn; v += kThreads)
+                lds_half[v] = __builtin_nontemporal_load(src + h0 + v);
+            __syncthreads();
+            const int seg = hn / 8, sg = tid / kPer, off = tid % kPer;
+            for (int i = 0; i * kPer < seg; ++i) {
+                const int v = sg * seg + i * kPer + off;
+                __builtin_nontemporal_store(lds_half[v], dst + h0 + v);
+            }
+            __syncthreads();  // the next half overwrites the buffer
+        }
+        return;
+    }
     for (int v0 = static_cast<int>(threadIdx.x); v0 < nv; v0 += kThreads * kStateUnroll) {
         svec16 buf[kStateUnroll];
 #pragma unroll
@@ -98,7 +127,8 @@ hipError_t launch_state(const StateArgs &args, int64_t pieces, Direction dir, bo
     a.npieces = pieces;
     const int64_t grid = host_side && KVX_STATE_HOST_WGS > 0 ? std::min<int64_t>(pieces, KVX_STATE_HOST_WGS) : pieces;
     void *kargs[] = {&a};
-    return hipLaunchKernel(fn, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), kargs, 0, stream);
+    return hipLaunchKernel(fn, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), kargs, host_side ? 0u : kStateLds,
+                           stream);
 }
 
 }  // namespace kvx

@@ -1305,6 +1305,15 @@ def main():
         s.synchronize()
         restore.append(time.perf_counter() - w0)
     restore_128k = statistics.median(restore)
+    # The same restore through kv_load_noalloc (static device scratch, every copy and kernel on the
+    # caller's stream, nothing allocated): what the no-allocation variant costs.
+    restore_noalloc = []
+    for _ in range(3):
+        w0 = time.perf_counter()
+        kvx.kv_load_noalloc(rep_b.cache, t_b, n, pool, ids, s)
+        s.synchronize()
+        restore_noalloc.append(time.perf_counter() - w0)
+    log(f"[bench] restore 128k through kv_load_noalloc: {statistics.median(restore_noalloc):.4f} s")
     # The paper's shorter prompts (Sec. 4.2: 8k to 256k tokens): prefixes of the same stored chunks.
     # Stores of the same prefixes rewrite the same bytes into the same slots.
     restore_by_len, store_by_len = {}, {}
@@ -1461,6 +1470,7 @@ def main():
         "store_GBps": round(store_gbps, 3), "load_GBps": round(load_gbps, 3),
         "restore_s_128k": round(restore_128k, 4),
         "restore_s_256k": restore_256k,
+        "restore_s_128k_noalloc": round(statistics.median(restore_noalloc), 4),
         "restore_s_by_prefix_tokens": restore_by_len,
         "store_GBps_by_prefix_tokens": store_by_len,
         "spread": spread,

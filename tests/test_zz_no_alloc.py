@@ -122,3 +122,45 @@ def test_noalloc_refuses_what_it_cannot_do():
         _noalloc(c, torch.zeros(8, dtype=torch.int32, device=DEV), 16, dpool, [0], s)
     assert e.value.status == kvx.KV_EINVAL
     kvx.kv_pool_destroy(dpool)
+
+
+def test_noalloc_replays_under_graph_capture():
+    """The callers this entry point is for include code under graph capture: the restore is captured
+    into a HIP graph and replayed three times, with eager work and synchronisation between the
+    replays; every replay must leave exactly kv_load's result (checked after each replay)."""
+    lay, NB = TINY, 512
+    seed = harness.sub_seed("noalloc", "graph")
+    A = host_cache(lay, NB, seed, "raw")
+    n = 4096 + 192
+    nc = lay.nc(n)
+    cid = harness.chunk_ids(nc, nc + 2, seed + 3)
+    pool = kvx.kv_pool_create(lay.kv, nc + 2, "staged")
+    dA = to_device(A)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    kvx.kv_store(kvx.Cache(dA, lay.kv, NB), bt_tensor(harness.block_table(seed + 1, NB, lay.nblk(n))), n, pool, cid, s)
+    tB = bt_tensor(harness.block_table(seed + 2, NB, lay.nblk(n)))
+    ref = torch.empty_like(dA)
+    ref.view(torch.uint8).fill_(SENT)
+    got = torch.empty_like(dA)
+    other = torch.empty_like(dA)
+    cache_got = kvx.Cache(got, lay.kv, NB)
+    torch.cuda.synchronize()
+    kvx.kv_load(kvx.Cache(ref, lay.kv, NB), tB, n, pool, cid, s)
+    _noalloc(cache_got, tB, n, pool, cid, s)  # first call on the device (address lookup) outside the capture
+    s.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        _noalloc(cache_got, tB, n, pool, cid, s)
+    t_other = bt_tensor(harness.block_table(seed + 4, NB, lay.nblk(n)))
+    for rep in range(3):
+        got.view(torch.uint8).fill_(SENT)
+        # Eager work of the program between replays: a restore of the same chunks elsewhere.
+        kvx.kv_load(kvx.Cache(other, lay.kv, NB), t_other, n, pool, cid, s)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref), f"replay {rep}: the captured restore differs from kv_load"
+    assert kvx.kv_pool_async_error(pool) == 0
+    del g
+    kvx.kv_pool_destroy(pool)

@@ -468,8 +468,10 @@ def start_replica(flag, sock, timeout=300):
 
 
 def stop_replica(proc):
-    proc.stdin.close()
+    if proc is None or proc.poll() is not None:
+        return
     try:
+        proc.stdin.close()
         proc.wait(timeout=60)
     except Exception:
         proc.kill()
@@ -488,6 +490,7 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
     tier = subprocess.Popen([sys.executable, "-u", me, "--tier-server", sock, "--mode", mode,
                              *(["--tier-load-mode", load_mode] if load_mode else [])],
                             stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+    rep_a = None
     try:
         line = tier.stdout.readline()
         if not line.startswith("READY"):
@@ -514,6 +517,7 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
         tier_out = json.loads(out.strip().splitlines()[-1])
         kern = tier_out["kernels"]
     finally:
+        stop_replica(rep_a)
         if tier.poll() is None:
             tier.kill()
     class PerLayer:  # the sampled check's view of per-layer buffers
@@ -615,6 +619,7 @@ def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=N
     tier = subprocess.Popen([sys.executable, "-u", me, "--paper-hybrid-server", sock, "--mode", mode,
                              *(["--tier-load-mode", load_mode] if load_mode else [])],
                             stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+    rep_a = None
     try:
         if not tier.stdout.readline().startswith("READY"):
             raise RuntimeError("tier did not start: " + tier.stderr.read()[-2000:])
@@ -639,6 +644,7 @@ def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=N
             raise RuntimeError("tier failed: " + (out + err)[-2000:])
         tier_out = json.loads(out.strip().splitlines()[-1])
     finally:
+        stop_replica(rep_a)
         if tier.poll() is None:
             tier.kill()
     # Checks: the snapshot pages equal A's page 1 (regenerated), and sampled hit chunks equal A's

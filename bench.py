@@ -452,9 +452,10 @@ def tier_store(np, torch, harness, hg, kvx, sock, dev):
 def start_replica(flag, sock, timeout=300):
     """Replica A in its own process: it stores through the tier, prints its result and stays alive,
     holding its cache, until its stdin closes.  Both replicas of the paper are long-lived; a replica
-    process that exited right after its store would free tens of GiB of device memory just before B's
-    restore, and the driver's clearing of freed device memory slows DMA copies for seconds (128k
-    restores measured 0.742 s instead of 0.603 s after a 32 GiB free).  Returns (process, result)."""
+    process that exited right after its store would free tens of GiB of device memory just before
+    B's restore, and the amdgpu kernel driver's clearing of freed device memory slows DMA copies for
+    seconds (128k restores measured 0.742 s instead of 0.603 s after a 32 GiB free).  Returns
+    (process, result)."""
     import select
     import subprocess
     proc = subprocess.Popen([sys.executable, "-u", os.path.abspath(__file__), flag, sock], stdin=subprocess.PIPE,
@@ -536,7 +537,8 @@ def tier_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=None):
                         "through a tier process that owns the pinned pool and its index; replica B (another "
                         "process) asks for the same prompt and restores its external hit; caches shared by HIP IPC, "
                         "one allocation per layer; host-side completion at both ends",
-            "mode": mode if not load_mode else f"{mode} stores, {load_mode} loads", "stored_chunks": a_out["stored_chunks"], "external_hit_tokens": hits[0],
+            "mode": mode if not load_mode else f"{mode} stores, {load_mode} loads",
+            "stored_chunks": a_out["stored_chunks"], "external_hit_tokens": hits[0],
             "store_s": round(store_s, 4), "store_GBps": round(N / store_s / 1e9, 3),
             "restore_s_first": round(restore[0], 4), "restore_s": round(statistics.median(restore[1:] or restore), 4),
             "restore_GBps": round(N / statistics.median(restore[1:] or restore) / 1e9, 3),
@@ -669,7 +671,8 @@ def paper_hybrid_leg(np, torch, harness, hg, kvx, mode, dev, reps=3, load_mode=N
                         "(4 KV heads, head_dim 256, 32-token HND pages), 1,568-token chunks, 48 recurrent layers with "
                         "3 MiB + 60 KiB snapshot pages; a 128,000-token prompt stored by replica A with its boundary "
                         "snapshot and restored by replica B under aligned recovery",
-            "mode": mode if not load_mode else f"{mode} stores, {load_mode} loads", "external_hit_tokens": hits[0], "stored_chunks": a_out["stored_chunks"],
+            "mode": mode if not load_mode else f"{mode} stores, {load_mode} loads",
+            "external_hit_tokens": hits[0], "stored_chunks": a_out["stored_chunks"],
             "bytes_restored": attn + snap, "store_s": round(a_out["store_s"], 4),
             "restore_s_first": round(restore[0], 4), "restore_s": round(med, 4),
             "restore_GBps": round((attn + snap) / med / 1e9, 3), "tier_index": tier_out["index"],
@@ -1192,7 +1195,8 @@ def main():
         tier, tier_ok = child_leg("--tier-only")
         if "error" not in tier:
             for m, t in tier.items():
-                log(f"[bench] tier ({m}, 3 processes): {t['external_hit_tokens']} tokens hit; store {t['store_s']} s ({t['store_GBps']} GB/s), restore "
+                log(f"[bench] tier ({m}, 3 processes): {t['external_hit_tokens']} tokens hit; "
+                    f"store {t['store_s']} s ({t['store_GBps']} GB/s), restore "
                     f"{t['restore_s']} s ({t['restore_GBps']} GB/s, first {t['restore_s_first']} s); "
                     f"{t['round_trip']}")
     hybrid, hybrid_ok = None, True

@@ -29,6 +29,13 @@ MUTANTS = {
                               "return b * block_stride + ((kv * BS + s) * H + h) * row_bytes;"),
     "nhd_read_as_hnd": ("return b * block_stride + ((kv * BS + s) * H + h) * row_bytes;",
                         "return b * block_stride + ((kv * H + h) * BS + s) * row_bytes;"),
+    "nhd_block_stride_ignored": ("return b * block_stride + ((kv * BS + s) * H + h) * row_bytes;",
+                                 "return b * (2 * H * BS * row_bytes) + ((kv * BS + s) * H + h) * row_bytes;"),
+    "duplicate_store_slots_accepted": ("    if (for_pack) {\n        /* Two chunks", "    if (0) {\n        /* Two chunks"),
+    "chunk_ids_ignored": ("uint8_t *slot = job->pool + job->chunk_ids[i] * slot_bytes;",
+                          "uint8_t *slot = job->pool + i * slot_bytes;"),
+    "last_block_id_unchecked": ("for (int64_t k = 0; k < n_blocks_used; ++k)",
+                                "for (int64_t k = 0; k + 1 < n_blocks_used; ++k)"),
     "state_layer_offset_dropped": ("uint8_t *packed = slot + g * page_bytes;", "uint8_t *packed = slot;"),
     "state_page_stride_ignored": ("state_layers[g] + pages[k] * page_stride;",
                                   "state_layers[g] + pages[k] * page_bytes;"),

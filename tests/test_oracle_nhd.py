@@ -80,6 +80,38 @@ def test_nhd_and_hnd_pack_the_same_tokens_identically():
     assert np.all(B[mask] == 0x11111111)
 
 
+def test_nhd_padded_block_stride():
+    """Token-major blocks with a block stride larger than one block: the pool holds each block's
+    unpadded token rows, and unpack writes no padding byte."""
+    L, H, D, E, BS, C = 2, 3, 4, 4, 4, 8
+    NB, pad = 9, 20  # extra 4-byte words after each block
+    blk = 2 * BS * H * D
+    rng = np.random.default_rng(17)
+    raw = rng.integers(0, 1 << 32, size=(L, NB, blk + pad), dtype=np.uint64).astype(np.uint32)
+    n = 21
+    nblk = -(-n // BS)
+    bt = rng.permutation(NB)[:nblk].astype(np.int32)
+    lay = oracle.make_layout(L, H, D, E, BS, C)
+    sb = oracle.slot_bytes(lay)
+    stride = (blk + pad) * E
+    pool = np.full(3 * sb, SENT, dtype=np.uint8)
+    ids = np.array([2, 0, 1])
+    layers = [raw[l].reshape(-1).view(np.uint8) for l in range(L)]
+    assert oracle.pack(lay, layers, stride, NB, bt, n, pool, ids, block_order=oracle.BLOCK_NHD) == oracle.OK
+    A = np.ascontiguousarray(raw[:, :, :blk]).reshape(L, NB, 2, BS, H, D)
+    tv = token_view_nhd(A, bt, n, BS)
+    for i in range(3):
+        ch = np.ascontiguousarray(tv[:, :, i * C:i * C + C])
+        got = pool[ids[i] * sb:ids[i] * sb + ch.nbytes].view(np.uint32).reshape(ch.shape)
+        np.testing.assert_array_equal(got, ch)
+    out = np.full_like(raw, 0x5A5A5A5A)
+    layers_out = [out[l].reshape(-1).view(np.uint8) for l in range(L)]
+    assert oracle.unpack(lay, layers_out, stride, NB, bt, n, pool, ids, block_order=oracle.BLOCK_NHD) == oracle.OK
+    assert np.all(out[:, :, blk:] == 0x5A5A5A5A)
+    B = np.ascontiguousarray(out[:, :, :blk]).reshape(L, NB, 2, BS, H, D)
+    np.testing.assert_array_equal(token_view_nhd(B, bt, n, BS), tv)
+
+
 def test_nhd_tags_paper_geometry():
     """The paper's attention geometry (FP8-sized 1-byte elements, 32-token pages, 1,568-token chunks,
     Sec. 3.1 / Table 1) in an NHD cache; E = 4 tags keep every word unique."""

@@ -267,9 +267,18 @@ def test_validation_rejects():
     assert oracle.validate(lay, 16, bs - 16, bt, 256, 1, cid, True) == oracle.EINVAL
     assert oracle.validate(lay, 15, bs, bt, 256, 1, cid, True) == oracle.EINVAL      # bt entry 15 out of range
     assert oracle.validate(lay, 16, bs, bt, 256, 1, np.array([1]), True) == oracle.EINVAL  # slot out of range
-    assert oracle.validate(lay, 16, bs, bt, 512, 2, np.array([1, 1]), True) == oracle.EINVAL   # duplicate store slot
+    # Two chunks stored into one slot would leave the slot order dependent (last writer wins), so a
+    # store naming a slot twice is refused; a load may read one slot into two places.  Every other
+    # argument is valid here, so the duplicate is the only reason for the refusal.
     bt2 = np.arange(32, dtype=np.int32)
+    assert oracle.validate(lay, 32, bs, bt2, 512, 2, np.array([0, 1]), True) == oracle.OK
+    assert oracle.validate(lay, 32, bs, bt2, 512, 2, np.array([1, 1]), True) == oracle.EINVAL   # duplicate store slot
     assert oracle.validate(lay, 32, bs, bt2, 512, 2, np.array([1, 1]), False) == oracle.OK  # duplicate load slot
+    A = np.zeros((2, 32, 2, 2, 16, 64), dtype=np.uint16)
+    pool = np.full(2 * oracle.slot_bytes(lay), SENT, dtype=np.uint8)
+    assert oracle.pack(lay, [A[l].reshape(-1).view(np.uint8) for l in range(2)], bs, 32, bt2, 512, pool,
+                       [1, 1]) == oracle.EINVAL
+    assert np.all(pool == SENT)  # refused before any byte moves
     assert oracle.validate(oracle.make_layout(2, 2, 64, 3, 16, 256), 16, 3 * bs, bt, 256, 1, cid, True) == oracle.EINVAL
     # Sec. 3.1: a chunk must be a whole number of pages; 1,568 tokens over 48-token pages is not.
     assert oracle.validate(oracle.make_layout(1, 1, 8, 1, 48, 1568), 64, 2 * 48 * 8, bt, 0, 0, None, True) == oracle.EINVAL

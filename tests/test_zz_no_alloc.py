@@ -1,7 +1,7 @@
 """kv_load_noalloc through the C ABI: the restore that allocates nothing (static device scratch,
 every copy and kernel on the caller's stream) must give exactly kv_load's result on the same inputs,
 on two calls in a row, the second with a smaller input.  Bit-exact (the path moves opaque bytes); the
-tiny case is also compared with the CPU oracle."""
+tiny case and 24 seeded random layouts are also compared with the CPU oracle."""
 import ctypes
 
 import numpy as np
@@ -9,6 +9,7 @@ import pytest
 import torch
 
 import harness
+import oracle
 from harness import gpu as hg
 from paper_2609_15021_amd import kvx
 from tests.gpu_support import (B27, DEV, TINY, bt_tensor, first_mismatch, host_cache, oracle_pool,
@@ -100,6 +101,44 @@ def test_noalloc_matches_kv_load_27b():
         s.synchronize()
         assert torch.equal(got, ref), f"call {call} (n={n}): kv_load_noalloc differs from kv_load"
         del ref, got
+    assert kvx.kv_pool_async_error(pool) == 0
+    kvx.kv_pool_destroy(pool)
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_noalloc_random_layouts(i):
+    """Seeded random layouts (the random-layout parity cases' generator: 1-5 layers, 1-8 heads,
+    16-128-byte rows of 1-, 2- and 4-byte elements, 1-32-token blocks, packed and padded strides,
+    both block orders, partial chunks, shuffled ids), the pool filled with the CPU oracle's packed
+    bytes: a restore of the whole prefix, then a shorter one into another cache; each equals the
+    oracle's cache bytes, sentinels included."""
+    from tests.test_gpu_fuzz import ORDERS, _case
+    lay, n, NB, stride, order, num_slots, _ = _case(i)
+    mode = ("staged", "zero_copy")[i % 2]
+    print(f"[noalloc] case {i} {mode}: L{lay.L} H{lay.H} D{lay.D} E{lay.E} BS{lay.BS} C{lay.C} n={n} NB={NB} "
+          f"stride={stride} order={order} slots={num_slots}", flush=True)
+    seed = harness.sub_seed("noalloc-fuzz", i)
+    rng = np.random.default_rng(seed)
+    A = [rng.integers(0, 256, NB * stride, dtype=np.uint8) for _ in range(lay.L)]
+    btA = harness.block_table(seed + 1, NB, lay.nblk(n))
+    ids = harness.chunk_ids(lay.nc(n), num_slots, seed + 3)
+    want_pool = np.full(num_slots * lay.slot_bytes, 0xA5, dtype=np.uint8)
+    assert oracle.pack(lay.orc, A, stride, NB, btA, n, want_pool, ids, 4, block_order=ORDERS[order]) == oracle.OK
+    pool = kvx.kv_pool_create(lay.kv, num_slots, mode)
+    kvx.pool_view(pool)[:] = want_pool
+    s = torch.cuda.Stream()
+    for call, m in enumerate((n, max(1, n // 3))):
+        btB = harness.block_table(seed + 10 + call, NB, lay.nblk(m))
+        want = [np.full(NB * stride, SENT, dtype=np.uint8) for _ in range(lay.L)]
+        assert oracle.unpack(lay.orc, want, stride, NB, btB, m, want_pool, ids[:lay.nc(m)], 4,
+                             block_order=ORDERS[order]) == oracle.OK
+        dB = [torch.full((NB * stride,), SENT, dtype=torch.uint8, device=DEV) for _ in range(lay.L)]
+        torch.cuda.synchronize()
+        _noalloc(kvx.Cache(dB, lay.kv, NB, stride, order), bt_tensor(btB), m, pool, ids[:lay.nc(m)], s)
+        s.synchronize()
+        for l in range(lay.L):
+            got = dB[l].cpu().numpy()
+            assert np.array_equal(got, want[l]), f"call {call} (n={m}) layer {l}: " + first_mismatch(got, want[l])
     assert kvx.kv_pool_async_error(pool) == 0
     kvx.kv_pool_destroy(pool)
 

@@ -90,6 +90,14 @@ kv_status release(kv_pool *p) {
         note(hipEventSynchronize(use.second), "hipEventSynchronize(last use)");
     for (auto &use : p->last_use)
         note(hipEventDestroy(use.second), "hipEventDestroy");
+    if (p->tier_stream) {
+        note(hipStreamSynchronize(p->tier_stream), "hipStreamSynchronize(tier)");
+        note(hipStreamDestroy(p->tier_stream), "hipStreamDestroy(tier)");
+    }
+    if (p->tier_table)
+        note(hipFree(p->tier_table), "hipFree(tier table)");
+    if (p->tier_table_pinned)
+        note(hipHostFree(p->tier_table_pinned), "hipHostFree(tier table)");
     for (auto &lane : p->lane) {
         for (hipStream_t s : lane.sides)
             note(hipStreamSynchronize(s), "hipStreamSynchronize(side)");

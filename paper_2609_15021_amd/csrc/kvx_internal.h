@@ -191,4 +191,18 @@ struct kv_pool {
 
     std::mutex mu;
     std::mutex tier_mu;  // serialises tier requests (one request's faults are its own)
+    // Tier serving: every request runs under tier_mu on this one stream, its block table staged
+    // through these buffers.  Made by the first request (or by kv_tier_run before it accepts a
+    // connection) and kept until kv_pool_destroy, so later connections create no runtime objects
+    // (a new stream and its first copy measured tens of ms on the request's path).
+    hipStream_t tier_stream = nullptr;
+    int32_t *tier_table = nullptr;         // device copy of the request's block table
+    int32_t *tier_table_pinned = nullptr;  // pinned host staging of it
+    size_t tier_table_cap = 0;             // bytes of each
 };
+
+namespace kvx {
+// Make the pool's tier stream and block-table buffers (at least `table_bytes` each) if they are
+// missing or too small.  Caller holds pool->tier_mu and has made the pool's device current.
+kv_status tier_resources(kv_pool *pool, size_t table_bytes);
+}  // namespace kvx

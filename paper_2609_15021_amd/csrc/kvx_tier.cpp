@@ -18,6 +18,7 @@
 #include <sys/un.h>
 #include <unistd.h>
 
+#include <algorithm>
 #include <array>
 #include <cerrno>
 #include <cstring>
@@ -115,21 +116,19 @@ class Connection {
     Connection(kv_pool *pool, kv_index *index, int fd) : pool_(pool), index_(index), fd_(fd) {}
 
     ~Connection() {
-        if (stream_) {
-            (void)hipStreamSynchronize(stream_);
-            (void)hipStreamDestroy(stream_);
+        // Every request completed on the tier stream before its reply; the wait below only
+        // guards the mappings against work a failed request might have left behind.
+        if (!opened_.empty()) {
+            std::lock_guard<std::mutex> lock(pool_->tier_mu);
+            if (pool_->tier_stream)
+                (void)hipStreamSynchronize(pool_->tier_stream);
+            for (auto &kv : opened_)
+                (void)hipIpcCloseMemHandle(kv.second.base);
         }
-        for (auto &kv : opened_)
-            (void)hipIpcCloseMemHandle(kv.second.base);
-        if (table_)
-            (void)hipFree(table_);
-        if (table_pinned_)
-            (void)hipHostFree(table_pinned_);
     }
 
     kv_status serve() {
         KVX_HIP(hipSetDevice(pool_->device));
-        KVX_HIP(hipStreamCreateWithFlags(&stream_, hipStreamNonBlocking));
         for (;;) {
             RequestHeader h;
             bool eof = false;
@@ -167,7 +166,12 @@ class Connection {
             int64_t value = 0, value2 = 0;
             {
                 std::lock_guard<std::mutex> lock(pool_->tier_mu);
-                st = execute(h, &value, &value2);
+                st = kvx::tier_resources(pool_, table_host_.size() * sizeof(int32_t));
+                if (st == KV_OK) {
+                    stream_ = pool_->tier_stream;
+                    table_ = pool_->tier_table;
+                    st = execute(h, &value, &value2);
+                }
             }
             const std::string msg = st == KV_OK ? std::string() : std::string(kv_last_error());
             ReplyHeader r{kMagic, st, static_cast<uint32_t>(msg.size()), 0, value, value2};
@@ -258,24 +262,13 @@ class Connection {
                 return st;
         }
 
-        // The block table into device memory on this connection's stream, from pinned host
-        // memory (an asynchronous copy from pageable memory would take the runtime's staged path).
+        // The block table into device memory on the tier stream, from pinned host memory (an
+        // asynchronous copy from pageable memory would take the runtime's staged path).  The
+        // previous request completed before its reply, so the staging is free.
         const size_t table_bytes = table_host_.size() * sizeof(int32_t);
-        if (table_bytes > table_cap_) {
-            if (table_)
-                KVX_HIP(hipFree(table_));
-            if (table_pinned_)
-                KVX_HIP(hipHostFree(table_pinned_));
-            table_ = nullptr;
-            table_pinned_ = nullptr;
-            table_cap_ = 0;
-            KVX_HIP(hipMalloc(reinterpret_cast<void **>(&table_), table_bytes));
-            KVX_HIP(hipHostMalloc(reinterpret_cast<void **>(&table_pinned_), table_bytes, hipHostMallocDefault));
-            table_cap_ = table_bytes;
-        }
         if (table_bytes) {
-            std::memcpy(table_pinned_, table_host_.data(), table_bytes);
-            KVX_HIP(hipMemcpyAsync(table_, table_pinned_, table_bytes, hipMemcpyHostToDevice, stream_));
+            std::memcpy(pool_->tier_table_pinned, table_host_.data(), table_bytes);
+            KVX_HIP(hipMemcpyAsync(table_, pool_->tier_table_pinned, table_bytes, hipMemcpyHostToDevice, stream_));
         }
 
         std::memset(cache, 0, sizeof(*cache));
@@ -430,10 +423,8 @@ class Connection {
     kv_pool *pool_;
     kv_index *index_;
     int fd_;
-    hipStream_t stream_ = nullptr;
+    hipStream_t stream_ = nullptr;  // the pool's tier stream and table, set for each request
     int32_t *table_ = nullptr;
-    int32_t *table_pinned_ = nullptr;  // host staging of the table (the previous request has completed)
-    size_t table_cap_ = 0;
     struct Mapping {
         void *base;
         int64_t bytes;
@@ -447,6 +438,34 @@ class Connection {
     std::vector<uint8_t> is_new_;
     std::vector<void *> layers_, state_layers_;
 };
+
+}  // namespace
+
+namespace kvx {
+
+kv_status tier_resources(kv_pool *pool, size_t table_bytes) {
+    if (!pool->tier_stream)
+        KVX_HIP(hipStreamCreateWithFlags(&pool->tier_stream, hipStreamNonBlocking));
+    if (table_bytes > pool->tier_table_cap) {
+        // Grow both buffers (the previous request has completed: nothing reads them).
+        const size_t cap = std::max<size_t>(table_bytes, size_t{1} << 20);
+        if (pool->tier_table)
+            KVX_HIP(hipFree(pool->tier_table));
+        if (pool->tier_table_pinned)
+            KVX_HIP(hipHostFree(pool->tier_table_pinned));
+        pool->tier_table = nullptr;
+        pool->tier_table_pinned = nullptr;
+        pool->tier_table_cap = 0;
+        KVX_HIP(hipMalloc(reinterpret_cast<void **>(&pool->tier_table), cap));
+        KVX_HIP(hipHostMalloc(reinterpret_cast<void **>(&pool->tier_table_pinned), cap, hipHostMallocDefault));
+        pool->tier_table_cap = cap;
+    }
+    return KV_OK;
+}
+
+}  // namespace kvx
+
+namespace {
 
 kv_status send_request(uint32_t op, int fd, const kv_cache *cache, const int32_t *block_table, int64_t n_tokens,
                        const int64_t *chunk_ids, uint64_t salt, const int32_t *tokens, const kv_state *state,
@@ -616,6 +635,23 @@ kv_status kv_tier_run(kv_pool *pool, kv_index *index, int listen_fd, int32_t con
             kv_status status = KV_OK;
             std::string message;
         };
+        // The tier stream and table buffers before the first connection, with one small copy on the
+        // stream: otherwise the first request pays for making them (tens of ms measured).
+        {
+            int prev = -1;
+            KVX_HIP(hipGetDevice(&prev));
+            KVX_HIP(hipSetDevice(pool->device));
+            std::lock_guard<std::mutex> lock(pool->tier_mu);
+            kv_status st = kvx::tier_resources(pool, sizeof(int32_t));
+            if (st == KV_OK) {
+                KVX_HIP(hipMemcpyAsync(pool->tier_table, pool->tier_table_pinned, sizeof(int32_t),
+                                       hipMemcpyHostToDevice, pool->tier_stream));
+                KVX_HIP(hipStreamSynchronize(pool->tier_stream));
+            }
+            KVX_HIP(hipSetDevice(prev));
+            if (st != KV_OK)
+                return st;
+        }
         std::deque<Result> results;  // push_back keeps references to earlier elements valid
         std::vector<std::thread> threads;
         kv_status accept_error = KV_OK;

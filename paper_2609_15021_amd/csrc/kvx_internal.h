@@ -22,7 +22,10 @@ constexpr int kMaxLaunchLayers = 64;   // layer pointers carried in one launch's
 constexpr int kMaxLaunchChunks = 256;  // slot ids carried in one launch's kernel arguments
 constexpr int kMaxStateLayers = 64;    // recurrent layers of a state snapshot (one launch carries all)
 constexpr int kMaxLaunchSnapshots = 128;  // snapshots carried in one state launch's arguments
-constexpr int64_t kStatePiece = 64 * 1024;  // bytes of a page one workgroup moves (at most)
+// Bytes of a page one workgroup moves (at most).  Paired on MI355X (48 x 3.06 MiB pages, device-side
+// launches, two orders): 16 KiB pieces moved 3.4-4.0% more on unpack than 64 KiB and the same as 32 KiB,
+// and pack followed (+5.5% over 64 KiB).
+constexpr int64_t kStatePiece = 16 * 1024;
 constexpr int64_t kMaxLaunchPieces = int64_t(1) << 22;  // workgroups of one state launch
 
 // Derived sizes of a layout (all bytes, 64-bit).

@@ -3,9 +3,9 @@
 // their device page buffers and the packed state slots, [G][page_bytes] per snapshot.
 //
 // Each page is contiguous on both sides, so the move is a batched copy: a workgroup moves
-// one piece (up to 64 KiB) of one page at a time with 16-byte vectors.  Device-side launches
-// run one workgroup per piece and pass it through LDS; host-side (zero-copy) launches run a
-// few workgroups that stride over the pieces and copy directly.
+// one piece (up to kStatePiece = 16 KiB) of one page at a time with 16-byte vectors.
+// Device-side launches run one workgroup per piece and pass it through LDS; host-side
+// (zero-copy) launches run a few workgroups that stride over the pieces and copy directly.
 // This work is bound by HBM (staging) or by
 // the host link (zero-copy); there is no arithmetic to put on the matrix cores.  Bytes
 // never pass through a float register.
@@ -45,17 +45,18 @@ __device__ __forceinline__ void move_piece(const StateArgs &a, int64_t q) {
     uint8_t *packed = a.base + a.off[k] + static_cast<int64_t>(g) * a.page_bytes + start;
     const svec16 *src = reinterpret_cast<const svec16 *>(DIR == kPack ? page : packed);
     svec16 *dst = reinterpret_cast<svec16 *>(DIR == kPack ? packed : page);
-    const int nv = static_cast<int>(len >> 4);  // len <= piece = 64 KiB
+    const int nv = static_cast<int>(len >> 4);  // len <= piece <= kStatePiece
     // Zero-copy stores into mapped pinned host memory use cache policy "nt sc1" (NT = 2, SC1 = 16),
     // as the gather kernels' do: over the link it moved more than plain nontemporal stores.
     const __amdgpu_buffer_rsrc_t dst_buf =
         __builtin_amdgcn_make_buffer_rsrc(dst, 0, static_cast<int>(len), 0x00020000);
 
     if constexpr (!HOST_SIDE) {
-        // Device-side launches move the piece through LDS in 32 KiB halves: contiguous reads into
-        // LDS, then writes with each pass spread over 8 segments of the half (512 B each).  Paired on
-        // 48 x 3.06 MiB pages, this moved 2.8-4.5% more (pack) and 3.9-4.0% more (unpack) than the
-        // direct copy with 4 vectors in flight; the LDS reservation alone changed nothing.
+        // Device-side launches move the piece through LDS, at most 32 KiB at a time: contiguous
+        // reads into LDS, then writes with each pass spread over 8 segments of what LDS holds.
+        // Paired on 48 x 3.06 MiB pages (then in 64 KiB pieces), this moved 2.8-4.5% more (pack)
+        // and 3.9-4.0% more (unpack) than the direct copy with 4 vectors in flight; the LDS
+        // reservation alone changed nothing.
         extern __shared__ svec16 lds_half[];
         constexpr int kHalf = kStateLds / 16, kPer = kThreads / 8;
         const int tid = static_cast<int>(threadIdx.x);

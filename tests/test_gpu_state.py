@@ -2,7 +2,7 @@
 
 Expected bytes come from the oracle's state pack/unpack applied to the same host-generated
 pages.  Cases cover snapshots smaller and larger than one staging slot, pages that are not a
-whole number of 64 KiB pieces, more snapshots than one launch carries, the maximum layer count,
+whole number of 16 KiB pieces, more snapshots than one launch carries, the maximum layer count,
 and a page geometry of a 27B-class hybrid model's recurrent layer.
 """
 import numpy as np

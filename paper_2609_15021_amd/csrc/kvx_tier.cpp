@@ -641,16 +641,24 @@ kv_status kv_tier_run(kv_pool *pool, kv_index *index, int listen_fd, int32_t con
             int prev = -1;
             KVX_HIP(hipGetDevice(&prev));
             KVX_HIP(hipSetDevice(pool->device));
-            std::lock_guard<std::mutex> lock(pool->tier_mu);
-            kv_status st = kvx::tier_resources(pool, sizeof(int32_t));
-            if (st == KV_OK) {
-                KVX_HIP(hipMemcpyAsync(pool->tier_table, pool->tier_table_pinned, sizeof(int32_t),
-                                       hipMemcpyHostToDevice, pool->tier_stream));
-                KVX_HIP(hipStreamSynchronize(pool->tier_stream));
+            kv_status st;
+            {
+                std::lock_guard<std::mutex> lock(pool->tier_mu);
+                st = kvx::tier_resources(pool, sizeof(int32_t));
+                hipError_t e = hipSuccess;
+                if (st == KV_OK)
+                    e = hipMemcpyAsync(pool->tier_table, pool->tier_table_pinned, sizeof(int32_t),
+                                       hipMemcpyHostToDevice, pool->tier_stream);
+                if (st == KV_OK && e == hipSuccess)
+                    e = hipStreamSynchronize(pool->tier_stream);
+                if (st == KV_OK && e != hipSuccess)
+                    st = kvx::hip_fail(e, "tier warm-up copy", __FILE__, __LINE__);
             }
-            KVX_HIP(hipSetDevice(prev));
+            const hipError_t e = hipSetDevice(prev);  // the caller's device, whatever happened above
             if (st != KV_OK)
                 return st;
+            if (e != hipSuccess)
+                return kvx::hip_fail(e, "hipSetDevice(caller's device)", __FILE__, __LINE__);
         }
         std::deque<Result> results;  // push_back keeps references to earlier elements valid
         std::vector<std::thread> threads;

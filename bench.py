@@ -1142,9 +1142,8 @@ def main():
         tier_store(np, torch, harness, hg, kvx, args.tier_store, dev)
         return
     if args.tier_only:
-        # Both modes: across processes zero-copy was measured faster than staged (the staged
-        # host-to-device copies slow down while kernels write IPC-imported caches).
-        # Also staged stores with zero-copy loads: the faster mode of each direction (one pool).
+        # Both modes, and staged stores with zero-copy loads (one pool), which measured the fastest
+        # restore across processes by a few ms.
         res, res_ok = {}, True
         for key, mode, load_mode in (("zero_copy", "zero_copy", None), ("staged", "staged", None),
                                      ("staged_store_zero_copy_load", "staged", "zero_copy")):

@@ -29,6 +29,22 @@ MUTANTS = {
             'for s in slots:\n            if s not in self.slot or self.slot[s]["pins"] == 0:'),
         "commit_allows_repeated_slots": ("if len(slots) != len(new) or len(set(slots)) != len(slots):",
                                          "if len(slots) != len(new):"),
+        "lookup_refreshes_past_the_hit": ("        self._touch_prefix(slots[:hit])", "        self._touch_prefix(slots)"),
+        "pending_snapshot_visible": (
+            'if self.slot[s]["state"] is not None and not self.slot[s]["state_pending"] else 0',
+            'if self.slot[s]["state"] is not None else 0'),
+        "abort_keeps_snapshot": ('                    e["aborted"] = True\n                    self._free_state_of(s)',
+                                 '                    e["aborted"] = True'),
+        "snapshot_evicted_under_pinned_owner": (
+            'if self.slot[owner]["pins"] == 0 and not self.slot[owner]["pending"]:',
+            'if not self.slot[owner]["pending"]:'),
+        "snapshot_lru_not_refreshed_by_hits": ("            self.state_lru.move_to_end(state_slot)\n", ""),
+        "snapshot_reserved_on_aborted_entry": (
+            'self.slot[s]["pins"] == 0 or self.slot[s]["aborted"]:\n            return EINVAL, -1, 0',
+            'self.slot[s]["pins"] == 0:\n            return EINVAL, -1, 0'),
+        "snapshot_abort_keeps_its_slot": (
+            '            ss = e["state"]\n            del self.state_owner[ss]\n            e["state"], e["state_pending"] = None, False',
+            '            ss = e["state"]\n            e["state"], e["state_pending"] = None, False'),
     },
 }
 

@@ -201,3 +201,83 @@ def test_commit_names_each_reserved_slot_once():
     assert [m.slot[s]["pins"] for s in slots] == [1, 1]   # the second replica's pins stand
     assert m.commit(slots2, new2, True) == 0
     assert [m.slot[s]["pins"] for s in slots] == [0, 0]
+
+
+def _store_with_snapshot(m, salt, toks, at):
+    """Store a prefix and the snapshot at the boundary after chunk `at` (both committed)."""
+    st, slots, new = m.reserve(salt, toks, len(toks))
+    assert st == 0
+    st, ss, is_new = m.reserve_state(slots[at])
+    assert st == 0 and is_new == 1
+    assert m.commit_state(slots[at]) == 0
+    assert m.commit(slots, new, True) == 0
+    return slots, ss
+
+
+def test_pending_snapshot_is_invisible():
+    """Sec. 3.2 (the host must see a store complete before anything reads it), applied to the
+    boundary snapshot: a reserved snapshot does not make a prefix restorable until it is committed."""
+    m = PoolIndexModel(4, 8, num_state_slots=2)
+    toks = list(range(8))
+    _store(m, 0, toks)
+    slots = m.lookup(0, toks, 8, pin=True)[2]
+    st, ss, is_new = m.reserve_state(slots[1])
+    assert st == 0 and is_new == 1
+    assert m.lookup(0, toks, 8, require_state=True)[1] == 0   # the snapshot is still pending
+    assert m.lookup(0, toks, 8)[1] == 2                        # the chunks alone are a hit
+    assert m.commit_state(slots[1]) == 0
+    kv, hit, _, got = m.lookup(0, toks, 8, require_state=True)
+    assert hit == 2 and got == ss
+    assert m.unpin(slots) == 0
+
+
+def test_aborted_store_frees_its_snapshot_and_takes_no_new_one():
+    """An aborted store publishes nothing (Sec. 3.2): its snapshot slot is freed with it, and an
+    aborted entry that another holder still pins cannot take a snapshot."""
+    m = PoolIndexModel(4, 8, num_state_slots=2)
+    toks = list(range(8))
+    st, slots, new = m.reserve(0, toks, 8)
+    assert m.reserve_state(slots[1])[0] == 0
+    assert m.stats()["free_state_slots"] == 1
+    st2, slots2, new2 = m.reserve(0, toks, 8)                  # a second replica holds the same entries
+    assert slots2 == slots and new2 == [0, 0]
+    assert m.commit(slots, new, False) == 0                   # the creator aborts
+    assert m.stats()["free_state_slots"] == 2
+    assert m.reserve_state(slots[1])[0] != 0                  # aborted, though still pinned
+    assert m.commit(slots2, new2, True) == 0                  # the other holder lets go
+    assert m.stats()["free_slots"] == 8 and m.lookup(0, toks, 8)[1] == 0
+
+
+def test_snapshot_lru_skips_pinned_owners_and_keeps_the_chunks():
+    """Snapshot slots have their own LRU (reading of Table 1's LRU for the snapshot budget): a hit
+    refreshes its snapshot, the least recently used snapshot of an unpinned entry is evicted first,
+    and evicting a snapshot keeps its chunk entry (still a hit without aligned recovery)."""
+    m = PoolIndexModel(2, 16, num_state_slots=2)
+    P1, P2, P3, P4 = ([k] * 2 for k in range(1, 5))
+    _store_with_snapshot(m, 0, P1, 0)
+    _store_with_snapshot(m, 0, P2, 0)
+    assert m.lookup(0, P1, 2, require_state=True)[1] == 1     # refreshes P1's snapshot
+    _store_with_snapshot(m, 0, P3, 0)                          # evicts P2's snapshot, not P1's
+    assert m.lookup(0, P2, 2, require_state=True)[1] == 0
+    assert m.lookup(0, P2, 2)[1] == 1
+    assert m.stats()["state_evictions"] == 1
+    held = m.lookup(0, P1, 2, pin=True)[2]                    # P1 pinned ...
+    assert m.lookup(0, P3, 2)[1] == 1                          # ... and now its snapshot is the older one
+    _store_with_snapshot(m, 0, P4, 0)                          # must evict P3's snapshot: P1's owner is pinned
+    assert m.lookup(0, P1, 2, require_state=True)[1] == 1
+    assert m.lookup(0, P3, 2, require_state=True)[1] == 0
+    assert m.unpin(held) == 0
+
+
+def test_lookup_refreshes_only_the_chunks_it_hits():
+    """LRU use is what a hit restores: with aligned recovery the hit stops at the last snapshot, and
+    the chunks past it are not refreshed, so they are evicted before another prompt's chunk."""
+    m = PoolIndexModel(2, 4, num_state_slots=1)
+    X = list(range(6))                                        # 3 chunks, snapshot after chunk 0
+    _store_with_snapshot(m, 0, X, 0)
+    Y = [50, 51]
+    _store(m, 0, Y)
+    assert m.lookup(0, X, 6, require_state=True)[1] == 1      # touches X's chunk 0 only
+    _store(m, 0, [60, 61])                                    # one eviction: X's chunk 2, the oldest
+    assert m.lookup(0, Y, 2)[1] == 1
+    assert m.lookup(0, X, 6)[1] == 2

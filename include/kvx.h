@@ -463,7 +463,9 @@ KV_API kv_status kv_index_get_stats(kv_index *index, kv_index_stats *out);
  *    and only then replies, so a stored chunk is committed (visible to any
  *    later request of any replica) and a loaded cache is complete when the
  *    call returns.
- * Requests from all connections to one pool are served one at a time.
+ * Requests from all connections to one pool are served one at a time, on one
+ * stream the pool keeps for this (made by kv_tier_run before it accepts a
+ * connection, or by the first request; released by kv_pool_destroy).
  * Device-side faults of a request (KV_ASYNC_*) are returned to its sender as
  * KV_EASYNC.
  * --------------------------------------------------------------------------- */

@@ -1232,7 +1232,9 @@ def main():
         f"(contiguous={info['staging_contiguous']})")
 
     peak = link_peak(torch, hg, info["host_base"], 1 << 30, dev)
-    log(f"[bench] pinned hipMemcpyAsync peak: D2H {peak['d2h']:.2f} GB/s, H2D {peak['h2d']:.2f} GB/s")
+    peak_chunk = link_peak(torch, hg, info["host_base"], 64 << 20, dev)  # one 27B-class chunk
+    log(f"[bench] pinned hipMemcpyAsync peak: D2H {peak['d2h']:.2f} GB/s, H2D {peak['h2d']:.2f} GB/s "
+        f"(64 MiB copies: {peak_chunk['d2h']:.2f} / {peak_chunk['h2d']:.2f})")
 
     s = torch.cuda.Stream()
 
@@ -1489,7 +1491,8 @@ def main():
         "link": {"peak_d2h_GBps": round(peak["d2h"], 3), "peak_h2d_GBps": round(peak["h2d"], 3),
                  "store_frac_of_peak": round(store_gbps / peak["d2h"], 4),
                  "load_frac_of_peak": round(load_gbps / peak["h2d"], 4),
-                 "peak_method": "median of 10 pinned hipMemcpyAsync of 1 GiB on the pool's own memory"},
+                 "peak_method": "median of 10 pinned hipMemcpyAsync of 1 GiB on the pool's own memory",
+                 "peak_64MiB_d2h_GBps": round(peak_chunk["d2h"], 3), "peak_64MiB_h2d_GBps": round(peak_chunk["h2d"], 3)},
         "roofline": roof,
         "concurrent_store_load": both,
         "zero_copy_compare": zc,

@@ -36,6 +36,15 @@ MUTANTS = {
                           "uint8_t *slot = job->pool + i * slot_bytes;"),
     "last_block_id_unchecked": ("for (int64_t k = 0; k < n_blocks_used; ++k)",
                                 "for (int64_t k = 0; k + 1 < n_blocks_used; ++k)"),
+    "cache_without_blocks_accepted": ("if (n_tokens < 0 || num_blocks <= 0 || num_slots < 0)",
+                                      "if (n_tokens < 0 || num_blocks < 0 || num_slots < 0)"),
+    "partial_chunk_last_token_dropped": ("for (int64_t u = 0; u < r; ++u) {", "for (int64_t u = 0; u + 1 < r; ++u) {"),
+    "slot_one_token_too_long": ("return (int64_t)lay->chunk_tokens * token_bytes;",
+                                "return (int64_t)(lay->chunk_tokens + 1) * token_bytes;"),
+    "state_load_slot_range_unchecked": (
+        "        if (slot_ids[k] < 0 || slot_ids[k] >= num_state_slots)\n            return ORACLE_EINVAL;",
+        "        if (for_pack && (slot_ids[k] < 0 || slot_ids[k] >= num_state_slots))\n            return ORACLE_EINVAL;"),
+    "state_null_layer_unchecked": ("    for (int64_t g = 0; g < num_layers; ++g)\n        if (!state_layers[g])\n            return ORACLE_EINVAL;", ""),
     "state_layer_offset_dropped": ("uint8_t *packed = slot + g * page_bytes;", "uint8_t *packed = slot;"),
     "state_page_stride_ignored": ("state_layers[g] + pages[k] * page_stride;",
                                   "state_layers[g] + pages[k] * page_bytes;"),

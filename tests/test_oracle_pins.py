@@ -266,6 +266,7 @@ def test_validation_rejects():
     assert oracle.validate(lay, 16, bs, bt, -1, 1, cid, True) == oracle.EINVAL
     assert oracle.validate(lay, 16, bs - 16, bt, 256, 1, cid, True) == oracle.EINVAL
     assert oracle.validate(lay, 15, bs, bt, 256, 1, cid, True) == oracle.EINVAL      # bt entry 15 out of range
+    assert oracle.validate(lay, 0, bs, None, 0, 1, None, True) == oracle.EINVAL     # a cache without blocks
     assert oracle.validate(lay, 16, bs, bt, 256, 1, np.array([1]), True) == oracle.EINVAL  # slot out of range
     # Two chunks stored into one slot would leave the slot order dependent (last writer wins), so a
     # store naming a slot twice is refused; a load may read one slot into two places.  Every other

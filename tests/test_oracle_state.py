@@ -103,6 +103,7 @@ def test_validation_rules():
     assert v(2, 16, 32, 4, [4], 1, 2, [0], True) == oracle.EINVAL               # page out of range
     assert v(2, 16, 32, 4, [-1], 1, 2, [0], True) == oracle.EINVAL
     assert v(2, 16, 32, 4, [0], 1, 2, [2], True) == oracle.EINVAL               # slot out of range
+    assert v(2, 16, 32, 4, [0], 1, 2, [2], False) == oracle.EINVAL              # ... for a load as well
     assert v(2, 16, 32, 4, [0, 1], 2, 2, [1, 1], True) == oracle.EINVAL         # store writes one slot twice
     assert v(2, 16, 32, 4, [0, 1], 2, 2, [1, 1], False) == oracle.OK            # a load may read it twice
     assert v(2, 16, 32, 4, [2, 2], 2, 2, [0, 1], False) == oracle.EINVAL        # load writes one page twice
@@ -116,3 +117,16 @@ def test_rejected_request_writes_nothing():
     pool = np.full(2 * 2 * 16, SENT, dtype=np.uint8)
     assert oracle.state_pack(_layers(A), 16, 16, [0, 1], pool, [1, 1]) == oracle.EINVAL
     assert (pool == SENT).all()
+
+
+def test_null_layer_pointer_rejected():
+    """A snapshot request whose layer list holds a NULL pointer is refused before any byte moves."""
+    import ctypes
+    A = np.arange(2 * 3 * 16, dtype=np.uint8).reshape(2, 3, 16)
+    pool = np.full(2 * 2 * 16, SENT, dtype=np.uint8)
+    layers = (ctypes.c_void_p * 2)(np.ascontiguousarray(A[0]).ctypes.data, None)
+    pages = np.array([0, 1], dtype=np.int64)
+    slots = np.array([0, 1], dtype=np.int64)
+    rc = oracle._load().oracle_state_pack(2, 16, 16, 3, layers, pages.ctypes.data, 2, pool.ctypes.data, 2,
+                                          slots.ctypes.data)
+    assert rc == oracle.EINVAL and (pool == SENT).all()

@@ -1351,8 +1351,9 @@ def main():
     log(f"[bench] store and load at once ({both['bytes_per_direction'] / 2**30:.0f} GiB each): "
         f"{both['aggregate_GBps']} GB/s in total (store {both['store_GBps']}, load {both['load_GBps']} GB/s)")
     # The same with staged stores and zero-copy loads: the load's kernels read the pool over the
-    # link on the caller's stream while the store's copies run on the side streams, so the two
-    # directions need not take turns on the side streams.
+    # link on the caller's stream while the store's copies run on its side stream, so the two
+    # directions never depend on which copy engines the runtime gives the two lanes' streams
+    # (staged both ways, some processes see both lanes' copies take turns).
     if args.mode == "staged" and info["staging_bytes"]:
         kvx.kv_pool_set_modes(pool, "staged", "zero_copy")
         both["staged_store_zero_copy_load"] = concurrent_leg(torch, kvx, rep_a, rep_b, t_a, t_b, n, ids, pool)
